@@ -1,0 +1,171 @@
+/*
+ * hs_merge.h -- C ABI of libhsmerge.so: merged retrieval on one MI355X (gfx950).
+ *
+ * Many concurrent workflows issue embedding-retrieval nodes over one shared
+ * chunk corpus.  Following HeraSys (Li et al.), Sec. 3.3 "Pre-Execution
+ * Optimization: Semantic Graph Fusion":
+ *   - each node carries a semantic signature (Eq. 2); nodes with equal
+ *     signatures are computationally equivalent;
+ *   - within a time window, a duplicate node is removed, its downstream edges
+ *     are redirected to the surviving node, and the survivor's output flows to
+ *     every related query (Topological Fusion within Time Window);
+ *   - same-type ready nodes execute as one batch (Appendix A, batching
+ *     constraint: b <= B_r, only nodes with consistent profile).
+ * The library runs that window as four device steps on a caller stream:
+ *   hs_dedup       group the R request keys (signatures) -> distinct keys,
+ *                  survivor per group, group sizes |M(v*)| (Eq. 3), and the
+ *                  redirect map request -> group;
+ *   hs_scatter     row gather: representative query rows, embedding rows of
+ *                  distinct chunk ids, and delivery of results to requests;
+ *   hs_score_topk  exact inner-product top-k of every distinct query against
+ *                  the corpus (retrieval with Top-K among its parameters,
+ *                  Eq. 2; top-K vector retrieval of the RAG workloads, Sec. 4.1)
+ *                  = hs_score_partial followed by hs_topk_merge.
+ *
+ * Conventions (all entry points):
+ *   - Every function returns hs_status.  Arguments are validated on the host
+ *     before anything is enqueued; on a non-OK status nothing was enqueued and
+ *     no output was written.  hs_last_error() gives a message (thread-local).
+ *   - Device pointers are plain addresses in the current HIP device's memory,
+ *     owned by the caller; the library never allocates or frees device memory
+ *     and keeps no pointer after a call returns.  Temporary device memory comes
+ *     from a caller-provided workspace (ws, ws_bytes) sized by hs_merge_plan.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     All work is asynchronous on that stream; outputs are valid after the
+ *     stream is synchronised.  The only host synchronisation the library ever
+ *     performs is the optional n_unique_host readback of hs_dedup.
+ *   - Layout: row-major and contiguous.  Row data pointers must be 16-byte
+ *     aligned; integer arrays must be aligned to their element size.
+ *   - Device-side faults (e.g. an out-of-range index inside device data) cannot
+ *     be reported synchronously: kernels skip such entries instead of reading
+ *     out of bounds, and document what they leave in the output.
+ */
+#ifndef HS_MERGE_H
+#define HS_MERGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HS_ABI_VERSION 1
+
+typedef enum {
+    HS_OK = 0,
+    HS_ERR_INVALID_ARG = 1,   /* null/negative/inconsistent argument */
+    HS_ERR_UNSUPPORTED = 2,   /* dtype / dim / k combination not implemented */
+    HS_ERR_WORKSPACE = 3,     /* workspace missing or smaller than required */
+    HS_ERR_ALIGNMENT = 4,     /* pointer not aligned as required */
+    HS_ERR_DEVICE = 5         /* a HIP call failed (message in hs_last_error) */
+} hs_status;
+
+typedef enum {
+    HS_F32 = 0,        /* IEEE binary32 */
+    HS_BF16 = 1,       /* bfloat16 (upper half of binary32), stored as uint16 */
+    HS_FP8_E4M3 = 2    /* OCP fp8 E4M3 ("fn": bias 7, max 448, no inf), uint8 */
+} hs_dtype;
+
+/* Shape of one merge window (one call sequence). */
+typedef struct {
+    int64_t n_requests;   /* R >= 0: retrieval nodes in the window, arrival order */
+    int64_t dim;          /* d: vector width; F32: d % 4 == 0, BF16: d % 8 == 0,
+                             FP8 corpus: d % 16 == 0; 1 <= d <= 16384 */
+    int64_t n_corpus;     /* N: corpus rows, 0 <= N <= 2^31 - 1 */
+    int32_t k;            /* results per node, 1 <= k <= 1024 (k > N pads) */
+    int32_t query_dtype;  /* HS_F32 or HS_BF16 */
+    int32_t corpus_dtype; /* HS_F32 (with F32 queries), HS_BF16 or HS_FP8_E4M3
+                             (with BF16 queries) */
+    int32_t flags;        /* reserved, must be 0 */
+    int64_t max_unique;   /* upper bound on distinct keys (0 = n_requests); the
+                             batch limit B_r of Appendix A when the caller sets it */
+} hs_merge_desc;
+
+typedef struct hs_plan hs_plan;   /* opaque, immutable, thread-safe host object */
+
+/* Validate `desc` and create a plan.  *workspace_bytes receives the size of the
+ * device workspace that hs_dedup and hs_score_topk (and its two phases) need
+ * for this shape.  The plan is freed with hs_plan_destroy. */
+hs_status hs_merge_plan(const hs_merge_desc *desc, hs_plan **plan, size_t *workspace_bytes);
+
+void hs_plan_destroy(hs_plan *plan);
+
+/* Step 1 -- signature matching (Sec. 3.3 (I); Appendix B.3, Phase 1: duplicate
+ * detection through a global duplication map).
+ *   keys          [R] int64 device: signature of request i (arrival order)
+ *   unique_keys   [R cap] int64 device out: distinct keys ascending (signed)
+ *   first_index   [R cap] int32 device out: earliest request of each group
+ *                 (the surviving node v_e)
+ *   counts        [R cap] int32 device out, may be NULL: group sizes |M(v*)|
+ *   inverse       [R] int32 device out: group of request i (redirected edge)
+ *   n_unique_dev  int64 device out: number of groups n_u
+ *   n_unique_host int64 host out, may be NULL: if given, the call waits for
+ *                 the stream once and stores n_u there
+ * Entries [n_u, R) of the per-group outputs are left unspecified.  R = 0 sets
+ * n_u = 0.  Bit-exact and deterministic. */
+hs_status hs_dedup(const hs_plan *plan, const int64_t *keys, int64_t *unique_keys,
+                   int32_t *first_index, int32_t *counts, int32_t *inverse,
+                   int64_t *n_unique_dev, int64_t *n_unique_host,
+                   void *ws, size_t ws_bytes, void *stream);
+
+/* Steps 3+4 -- one exact top-k retrieval per distinct node over the corpus.
+ *   q_unique      [n_u x d] device, query_dtype: representative query rows
+ *   n_unique      host count n_u, or -1 to read it from n_unique_dev on the
+ *                 device (the launch then covers max_unique rows)
+ *   n_unique_dev  int64 device, used when n_unique == -1 (else may be NULL)
+ *   corpus        [N x d] device, corpus_dtype
+ *   row_scale     [N] fp32 device: per-row dequantisation scale, FP8 only
+ *                 (score = row_scale[c] * <q, decode(C[c])>), else NULL
+ *   topk_score    [n_u x k] fp32 device out: best scores, descending
+ *   topk_index    [n_u x k] int32 device out: corpus rows; equal scores are
+ *                 ordered by ascending row; slots beyond N are (-inf, -1)
+ * Scores accumulate in fp32 from exact bf16/fp8 products (fp32 products for
+ * F32 inputs).  Identical corpus rows get bit-identical scores. */
+hs_status hs_score_topk(const hs_plan *plan, const void *q_unique, int64_t n_unique,
+                        const int64_t *n_unique_dev, const void *corpus,
+                        const float *row_scale, float *topk_score, int32_t *topk_index,
+                        void *ws, size_t ws_bytes, void *stream);
+
+/* Phase 1 of hs_score_topk: scores every distinct query against the corpus in
+ * one persistent kernel, each workgroup keeping the k best (score, row) pairs
+ * of its corpus slice per query; the per-slice lists go to the workspace.
+ * Arguments as for hs_score_topk. */
+hs_status hs_score_partial(const hs_plan *plan, const void *q_unique, int64_t n_unique,
+                           const int64_t *n_unique_dev, const void *corpus,
+                           const float *row_scale, void *ws, size_t ws_bytes, void *stream);
+
+/* Phase 2 of hs_score_topk: merges the per-slice lists left in the workspace
+ * by hs_score_partial (same plan, same n_unique arguments, same workspace)
+ * into the final sorted top-k per distinct query. */
+hs_status hs_topk_merge(const hs_plan *plan, int64_t n_unique, const int64_t *n_unique_dev,
+                        float *topk_score, int32_t *topk_index,
+                        void *ws, size_t ws_bytes, void *stream);
+
+/* Steps 2, 2' and 5 -- row gather dst[i] = src[index[i]], i < n_rows.
+ * The race-free form of delivering one result to many nodes (Sec. 3.3 (I):
+ * the survivor's output flows to all related queries):
+ *   representative rows: src = request queries,  index = first_index
+ *   embedding rows:      src = embedding table,  index = unique_keys (int64)
+ *   delivery:            src = topk_score/index, index = inverse
+ *   src        [src_rows x row_bytes] device
+ *   row_bytes  > 0 and a multiple of 4 (16-byte rows use 128-bit accesses)
+ *   index      [n_out] int32 (index_is_i64 = 0) or int64 (= 1) device
+ *   n_out      host row count (upper bound when n_out_dev is given)
+ *   n_out_dev  int64 device, may be NULL: actual row count (<= n_out), e.g.
+ *              n_unique_dev from hs_dedup
+ *   dst        [n_out x row_bytes] device out
+ * Rows whose index falls outside [0, src_rows) are left unwritten. */
+hs_status hs_scatter(const void *src, int64_t src_rows, int64_t row_bytes,
+                     const void *index, int32_t index_is_i64, int64_t n_out,
+                     const int64_t *n_out_dev, void *dst, void *stream);
+
+const char *hs_status_string(hs_status s);
+const char *hs_last_error(void);
+int32_t hs_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HS_MERGE_H */

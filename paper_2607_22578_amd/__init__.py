@@ -1,0 +1,255 @@
+"""Python binding of libhsmerge.so (merged retrieval on MI355X / gfx950).
+
+Argument marshalling only: every step runs in the HIP kernels of the shared
+library.  Functions carry the C names of include/hs_merge.h and take device
+buffers as torch tensors (or raw integer addresses); PyTorch serves only to
+own device memory and streams.  Importing fails loudly when the library has
+not been built -- there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhsmerge.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                      "(hipcc --offload-arch=gfx950)")
+
+# torch ships its own HIP runtime.  Load it first so that the library binds to
+# the same runtime instance (by soname) instead of bringing a second runtime
+# into the process; two runtimes cannot share the device.
+try:
+    import torch as _torch  # noqa: F401
+except ImportError:  # plain C-ABI use without torch
+    _torch = None
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+HS_OK, HS_ERR_INVALID_ARG, HS_ERR_UNSUPPORTED, HS_ERR_WORKSPACE, HS_ERR_ALIGNMENT, \
+    HS_ERR_DEVICE = range(6)
+HS_F32, HS_BF16, HS_FP8_E4M3 = 0, 1, 2
+ABI_VERSION = 1
+
+EXPORTS = ["hs_merge_plan", "hs_plan_destroy", "hs_dedup", "hs_score_topk", "hs_score_partial",
+           "hs_topk_merge", "hs_scatter", "hs_status_string", "hs_last_error", "hs_abi_version"]
+
+
+class hs_merge_desc(ctypes.Structure):
+    _fields_ = [("n_requests", ctypes.c_int64), ("dim", ctypes.c_int64),
+                ("n_corpus", ctypes.c_int64), ("k", ctypes.c_int32),
+                ("query_dtype", ctypes.c_int32), ("corpus_dtype", ctypes.c_int32),
+                ("flags", ctypes.c_int32), ("max_unique", ctypes.c_int64)]
+
+
+_vp, _i64, _i32, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+_lib.hs_merge_plan.argtypes = [ctypes.POINTER(hs_merge_desc), ctypes.POINTER(_vp),
+                               ctypes.POINTER(_sz)]
+_lib.hs_merge_plan.restype = ctypes.c_int
+_lib.hs_plan_destroy.argtypes = [_vp]
+_lib.hs_plan_destroy.restype = None
+_lib.hs_dedup.argtypes = [_vp] + [_vp] * 7 + [_vp, _sz, _vp]
+_lib.hs_dedup.restype = ctypes.c_int
+_lib.hs_score_topk.argtypes = [_vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+_lib.hs_score_topk.restype = ctypes.c_int
+_lib.hs_score_partial.argtypes = [_vp, _vp, _i64, _vp, _vp, _vp, _vp, _sz, _vp]
+_lib.hs_score_partial.restype = ctypes.c_int
+_lib.hs_topk_merge.argtypes = [_vp, _i64, _vp, _vp, _vp, _vp, _sz, _vp]
+_lib.hs_topk_merge.restype = ctypes.c_int
+_lib.hs_scatter.argtypes = [_vp, _i64, _i64, _vp, _i32, _i64, _vp, _vp, _vp]
+_lib.hs_scatter.restype = ctypes.c_int
+_lib.hs_status_string.argtypes = [ctypes.c_int]
+_lib.hs_status_string.restype = ctypes.c_char_p
+_lib.hs_last_error.argtypes = []
+_lib.hs_last_error.restype = ctypes.c_char_p
+_lib.hs_abi_version.argtypes = []
+_lib.hs_abi_version.restype = ctypes.c_int32
+
+
+class HsError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{hs_status_string(status)}: {msg}")
+        self.status = status
+
+
+def hs_status_string(status: int) -> str:
+    return _lib.hs_status_string(status).decode()
+
+
+def hs_last_error() -> str:
+    return _lib.hs_last_error().decode()
+
+
+def hs_abi_version() -> int:
+    return int(_lib.hs_abi_version())
+
+
+def _check(status: int):
+    if status != HS_OK:
+        raise HsError(status, hs_last_error())
+
+
+def _ptr(x):
+    """Device/host address of a torch tensor, an int address, or None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return None
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def dtype_code(t) -> int:
+    """HS dtype of a torch tensor (float32, bfloat16, uint8/float8_e4m3fn)."""
+    import torch
+    m = {torch.float32: HS_F32, torch.bfloat16: HS_BF16, torch.uint8: HS_FP8_E4M3,
+         torch.float8_e4m3fn: HS_FP8_E4M3}
+    if t.dtype not in m:
+        raise TypeError(f"unsupported dtype {t.dtype}")
+    return m[t.dtype]
+
+
+@dataclass
+class Plan:
+    handle: int
+    workspace_bytes: int
+    desc: hs_merge_desc
+
+    def __del__(self):
+        if self.handle:
+            _lib.hs_plan_destroy(self.handle)
+            self.handle = 0
+
+
+def hs_merge_plan(n_requests: int, dim: int, n_corpus: int, k: int, query_dtype: int,
+                  corpus_dtype: int, max_unique: int = 0, flags: int = 0) -> Plan:
+    d = hs_merge_desc(n_requests, dim, n_corpus, k, query_dtype, corpus_dtype, flags, max_unique)
+    h = _vp()
+    ws = _sz()
+    _check(_lib.hs_merge_plan(ctypes.byref(d), ctypes.byref(h), ctypes.byref(ws)))
+    return Plan(h.value, int(ws.value), d)
+
+
+def hs_dedup(plan: Plan, keys, unique_keys, first_index, counts, inverse, n_unique_dev,
+             n_unique_host=None, ws=None, ws_bytes: Optional[int] = None, stream=None):
+    host = None
+    if n_unique_host is True:
+        host = ctypes.c_int64(-1)
+        hptr = ctypes.addressof(host)
+    else:
+        hptr = _ptr(n_unique_host)
+    _check(_lib.hs_dedup(plan.handle, _ptr(keys), _ptr(unique_keys), _ptr(first_index),
+                         _ptr(counts), _ptr(inverse), _ptr(n_unique_dev), hptr, _ptr(ws),
+                         _ws_bytes(ws, ws_bytes), _stream(stream)))
+    return None if host is None else int(host.value)
+
+
+def _ws_bytes(ws, ws_bytes):
+    if ws_bytes is not None:
+        return ws_bytes
+    if ws is None or isinstance(ws, int):
+        return 0
+    return ws.numel() * ws.element_size()
+
+
+def hs_score_topk(plan: Plan, q_unique, n_unique: int, n_unique_dev, corpus, row_scale,
+                  topk_score, topk_index, ws=None, ws_bytes: Optional[int] = None, stream=None):
+    _check(_lib.hs_score_topk(plan.handle, _ptr(q_unique), n_unique, _ptr(n_unique_dev),
+                              _ptr(corpus), _ptr(row_scale), _ptr(topk_score), _ptr(topk_index),
+                              _ptr(ws), _ws_bytes(ws, ws_bytes), _stream(stream)))
+
+
+def hs_score_partial(plan: Plan, q_unique, n_unique: int, n_unique_dev, corpus, row_scale,
+                     ws=None, ws_bytes: Optional[int] = None, stream=None):
+    _check(_lib.hs_score_partial(plan.handle, _ptr(q_unique), n_unique, _ptr(n_unique_dev),
+                                 _ptr(corpus), _ptr(row_scale), _ptr(ws),
+                                 _ws_bytes(ws, ws_bytes), _stream(stream)))
+
+
+def hs_topk_merge(plan: Plan, n_unique: int, n_unique_dev, topk_score, topk_index, ws=None,
+                  ws_bytes: Optional[int] = None, stream=None):
+    _check(_lib.hs_topk_merge(plan.handle, n_unique, _ptr(n_unique_dev), _ptr(topk_score),
+                              _ptr(topk_index), _ptr(ws), _ws_bytes(ws, ws_bytes),
+                              _stream(stream)))
+
+
+def hs_scatter(src, src_rows: int, row_bytes: int, index, index_is_i64: int, n_out: int,
+               n_out_dev, dst, stream=None):
+    _check(_lib.hs_scatter(_ptr(src), src_rows, row_bytes, _ptr(index), index_is_i64, n_out,
+                           _ptr(n_out_dev), _ptr(dst), _stream(stream)))
+
+
+# ---------------------------------------------------------------- composition
+
+class MergedRetrieval:
+    """Owns the plan, workspace and per-window buffers for one shape and runs
+    the whole path (dedup -> representative rows -> score/top-k -> delivery)
+    on one stream.  All outputs are torch tensors on the device."""
+
+    def __init__(self, n_requests: int, dim: int, n_corpus: int, k: int, query_dtype: int,
+                 corpus_dtype: int, device="cuda", max_unique: int = 0):
+        import torch
+        self.R, self.d, self.N, self.k = n_requests, dim, n_corpus, k
+        self.qdt, self.cdt = query_dtype, corpus_dtype
+        self.plan = hs_merge_plan(n_requests, dim, n_corpus, k, query_dtype, corpus_dtype,
+                                  max_unique)
+        cap = max_unique if max_unique > 0 else n_requests
+        self.cap = cap
+        dev = torch.device(device)
+        R1 = max(n_requests, 1)
+        qt = torch.float32 if query_dtype == HS_F32 else torch.bfloat16
+        self.ws = torch.empty(max(self.plan.workspace_bytes, 256), dtype=torch.uint8, device=dev)
+        self.unique_keys = torch.empty(R1, dtype=torch.int64, device=dev)
+        self.first_index = torch.empty(R1, dtype=torch.int32, device=dev)
+        self.counts = torch.empty(R1, dtype=torch.int32, device=dev)
+        self.inverse = torch.empty(R1, dtype=torch.int32, device=dev)
+        self.n_unique = torch.zeros(1, dtype=torch.int64, device=dev)
+        self.q_unique = torch.empty((max(cap, 1), dim), dtype=qt, device=dev)
+        self.topk_score = torch.empty((max(cap, 1), k), dtype=torch.float32, device=dev)
+        self.topk_index = torch.empty((max(cap, 1), k), dtype=torch.int32, device=dev)
+        self.out_score = torch.empty((R1, k), dtype=torch.float32, device=dev)
+        self.out_index = torch.empty((R1, k), dtype=torch.int32, device=dev)
+        self.q_row_bytes = dim * (4 if query_dtype == HS_F32 else 2)
+
+    def dedup(self, keys, stream=None, host_count: bool = False):
+        return hs_dedup(self.plan, keys, self.unique_keys, self.first_index, self.counts,
+                        self.inverse, self.n_unique, True if host_count else None, self.ws,
+                        stream=stream)
+
+    def gather_queries(self, q_req, stream=None):
+        hs_scatter(q_req, self.R, self.q_row_bytes, self.first_index, 0, self.cap,
+                   self.n_unique, self.q_unique, stream=stream)
+
+    def score_partial(self, corpus, scale=None, n_unique: int = -1, stream=None):
+        hs_score_partial(self.plan, self.q_unique, n_unique, self.n_unique, corpus, scale,
+                         self.ws, stream=stream)
+
+    def topk_merge(self, n_unique: int = -1, stream=None):
+        hs_topk_merge(self.plan, n_unique, self.n_unique, self.topk_score, self.topk_index,
+                      self.ws, stream=stream)
+
+    def deliver(self, stream=None):
+        hs_scatter(self.topk_score, self.cap, self.k * 4, self.inverse, 0, self.R, None,
+                   self.out_score, stream=stream)
+        hs_scatter(self.topk_index, self.cap, self.k * 4, self.inverse, 0, self.R, None,
+                   self.out_index, stream=stream)
+
+    def run(self, keys, q_req, corpus, scale=None, stream=None, n_unique: int = -1):
+        """The whole window; n_unique = -1 keeps the distinct count on the
+        device (no host synchronisation)."""
+        self.dedup(keys, stream)
+        self.gather_queries(q_req, stream)
+        self.score_partial(corpus, scale, n_unique, stream)
+        self.topk_merge(n_unique, stream)
+        self.deliver(stream)

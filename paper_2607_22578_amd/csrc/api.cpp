@@ -1,0 +1,268 @@
+// Host side of libhsmerge: argument validation, plans, workspace layout and
+// kernel launches behind the C ABI declared in include/hs_merge.h.
+//
+// Every entry point validates all of its arguments before it enqueues
+// anything, so a non-OK status means nothing was launched and no output was
+// touched.  No entry point allocates device memory.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+
+#include "../../include/hs_merge.h"
+
+namespace hs {
+size_t dedup_workspace_bytes(int64_t R);
+hipError_t launch_dedup(const int64_t *keys, int64_t R, int64_t *uk, int32_t *fi, int32_t *cnt,
+                        int32_t *inv, int64_t *nu, void *ws, hipStream_t st);
+hipError_t launch_gather(const void *src, int64_t src_rows, int64_t row_bytes, const void *index,
+                         int is64, int64_t n_out, const int64_t *n_out_dev, void *dst,
+                         hipStream_t st);
+size_t score_workspace_bytes(int64_t cap, int64_t N, int k, int corpus_dtype);
+hipError_t launch_score_partial(const void *q, const void *corpus, const float *scale, int64_t N,
+                                int64_t d, int k, int64_t n_unique, const int64_t *nu_dev,
+                                int64_t cap, int corpus_dtype, void *part, hipStream_t st);
+hipError_t launch_topk_merge(const void *part, int64_t n_unique, const int64_t *nu_dev,
+                             int64_t cap, int64_t N, int k, int corpus_dtype, float *out_s,
+                             int32_t *out_i, hipStream_t st);
+}  // namespace hs
+
+struct hs_plan {
+  hs_merge_desc d;
+  int64_t cap;          // max distinct keys
+  size_t ws_dedup;      // bytes used by hs_dedup (offset 0)
+  size_t ws_score;      // bytes used by the score phases (offset 0)
+  size_t ws_total;
+};
+
+static thread_local char g_err[512];
+
+static hs_status fail(hs_status s, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+static hs_status ok() {
+  g_err[0] = 0;
+  return HS_OK;
+}
+
+static bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+static hs_status device_status(hipError_t e, const char *what) {
+  if (e == hipSuccess) return ok();
+  return fail(HS_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+extern "C" {
+
+int32_t hs_abi_version(void) { return HS_ABI_VERSION; }
+
+const char *hs_last_error(void) { return g_err; }
+
+const char *hs_status_string(hs_status s) {
+  switch (s) {
+    case HS_OK: return "HS_OK";
+    case HS_ERR_INVALID_ARG: return "HS_ERR_INVALID_ARG";
+    case HS_ERR_UNSUPPORTED: return "HS_ERR_UNSUPPORTED";
+    case HS_ERR_WORKSPACE: return "HS_ERR_WORKSPACE";
+    case HS_ERR_ALIGNMENT: return "HS_ERR_ALIGNMENT";
+    case HS_ERR_DEVICE: return "HS_ERR_DEVICE";
+  }
+  return "HS_ERR_UNKNOWN";
+}
+
+hs_status hs_merge_plan(const hs_merge_desc *desc, hs_plan **plan, size_t *workspace_bytes) {
+  if (!desc || !plan || !workspace_bytes)
+    return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: null argument");
+  const hs_merge_desc &d = *desc;
+  if (d.flags != 0) return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: flags must be 0");
+  if (d.n_requests < 0 || d.n_requests > INT32_MAX)
+    return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: n_requests %lld out of [0, 2^31-1]",
+                (long long)d.n_requests);
+  if (d.n_corpus < 0 || d.n_corpus > INT32_MAX)
+    return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: n_corpus %lld out of [0, 2^31-1]",
+                (long long)d.n_corpus);
+  if (d.dim < 1 || d.dim > 16384)
+    return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: dim %lld out of [1, 16384]",
+                (long long)d.dim);
+  if (d.k < 1 || d.k > 1024)
+    return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: k %d out of [1, 1024]", d.k);
+  if (d.max_unique < 0 || d.max_unique > d.n_requests)
+    return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: max_unique %lld out of [0, n_requests]",
+                (long long)d.max_unique);
+  const bool qf32 = d.query_dtype == HS_F32, qbf16 = d.query_dtype == HS_BF16;
+  if (!qf32 && !qbf16)
+    return fail(HS_ERR_UNSUPPORTED, "hs_merge_plan: query_dtype %d unsupported", d.query_dtype);
+  if (qf32 && d.corpus_dtype != HS_F32)
+    return fail(HS_ERR_UNSUPPORTED, "hs_merge_plan: F32 queries need an F32 corpus");
+  if (qbf16 && d.corpus_dtype != HS_BF16 && d.corpus_dtype != HS_FP8_E4M3)
+    return fail(HS_ERR_UNSUPPORTED, "hs_merge_plan: BF16 queries need a BF16 or FP8 corpus");
+  if (qf32 && d.dim % 4 != 0)
+    return fail(HS_ERR_UNSUPPORTED, "hs_merge_plan: F32 needs dim %% 4 == 0");
+  if (qbf16 && d.dim % 8 != 0)
+    return fail(HS_ERR_UNSUPPORTED, "hs_merge_plan: BF16 needs dim %% 8 == 0");
+  if (d.corpus_dtype == HS_FP8_E4M3 && d.dim % 16 != 0)
+    return fail(HS_ERR_UNSUPPORTED, "hs_merge_plan: FP8 corpus needs dim %% 16 == 0");
+  hs_plan *p = new (std::nothrow) hs_plan;
+  if (!p) return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: out of host memory");
+  p->d = d;
+  p->cap = d.max_unique > 0 ? d.max_unique : d.n_requests;
+  p->ws_dedup = hs::dedup_workspace_bytes(d.n_requests);
+  p->ws_score = hs::score_workspace_bytes(p->cap, d.n_corpus, d.k, d.corpus_dtype);
+  p->ws_total = p->ws_dedup > p->ws_score ? p->ws_dedup : p->ws_score;
+  *plan = p;
+  *workspace_bytes = p->ws_total;
+  return ok();
+}
+
+void hs_plan_destroy(hs_plan *plan) { delete plan; }
+
+hs_status hs_dedup(const hs_plan *plan, const int64_t *keys, int64_t *unique_keys,
+                   int32_t *first_index, int32_t *counts, int32_t *inverse,
+                   int64_t *n_unique_dev, int64_t *n_unique_host, void *ws, size_t ws_bytes,
+                   void *stream) {
+  if (!plan) return fail(HS_ERR_INVALID_ARG, "hs_dedup: null plan");
+  const int64_t R = plan->d.n_requests;
+  if (!n_unique_dev) return fail(HS_ERR_INVALID_ARG, "hs_dedup: null n_unique_dev");
+  if (R > 0 && (!keys || !unique_keys || !first_index || !inverse))
+    return fail(HS_ERR_INVALID_ARG, "hs_dedup: null array argument");
+  if (!aligned(keys, 8) || !aligned(unique_keys, 8) || !aligned(n_unique_dev, 8) ||
+      !aligned(first_index, 4) || !aligned(inverse, 4) || !aligned(counts, 4))
+    return fail(HS_ERR_ALIGNMENT, "hs_dedup: misaligned pointer");
+  if (plan->ws_dedup > 0 && (!ws || ws_bytes < plan->ws_dedup))
+    return fail(HS_ERR_WORKSPACE, "hs_dedup: workspace %zu bytes, need %zu", ws_bytes,
+                plan->ws_dedup);
+  if (plan->ws_dedup > 0 && !aligned(ws, 256))
+    return fail(HS_ERR_ALIGNMENT, "hs_dedup: workspace must be 256-byte aligned");
+  hipStream_t st = (hipStream_t)stream;
+  {
+    hipError_t e = hs::launch_dedup(keys, R, unique_keys, first_index, counts, inverse,
+                                    n_unique_dev, ws, st);
+    if (e != hipSuccess) return device_status(e, "hs_dedup launch");
+  }
+  if (n_unique_host) {
+    hipError_t e = hipMemcpyAsync(n_unique_host, n_unique_dev, sizeof(int64_t),
+                                  hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return device_status(e, "hs_dedup readback");
+  }
+  return ok();
+}
+
+static hs_status check_nu(const hs_plan *plan, int64_t n_unique, const int64_t *n_unique_dev,
+                          const char *who) {
+  if (n_unique == -1) {
+    if (!n_unique_dev) return fail(HS_ERR_INVALID_ARG, "%s: n_unique = -1 needs n_unique_dev", who);
+    if (!aligned(n_unique_dev, 8)) return fail(HS_ERR_ALIGNMENT, "%s: misaligned n_unique_dev", who);
+  } else if (n_unique < 0 || n_unique > plan->cap) {
+    return fail(HS_ERR_INVALID_ARG, "%s: n_unique %lld out of [0, %lld]", who,
+                (long long)n_unique, (long long)plan->cap);
+  }
+  return HS_OK;
+}
+
+static hs_status check_score_ws(const hs_plan *plan, void *ws, size_t ws_bytes, const char *who) {
+  if (plan->ws_score > 0 && (!ws || ws_bytes < plan->ws_score))
+    return fail(HS_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", who, ws_bytes,
+                plan->ws_score);
+  if (plan->ws_score > 0 && !aligned(ws, 256))
+    return fail(HS_ERR_ALIGNMENT, "%s: workspace must be 256-byte aligned", who);
+  return HS_OK;
+}
+
+static hs_status check_partial(const hs_plan *plan, const void *q_unique, int64_t n_unique,
+                               const int64_t *n_unique_dev, const void *corpus,
+                               const float *row_scale, void *ws, size_t ws_bytes,
+                               const char *who) {
+  hs_status s = check_nu(plan, n_unique, n_unique_dev, who);
+  if (s != HS_OK) return s;
+  const hs_merge_desc &d = plan->d;
+  if (!q_unique && n_unique != 0) return fail(HS_ERR_INVALID_ARG, "%s: null q_unique", who);
+  if (!corpus && d.n_corpus > 0) return fail(HS_ERR_INVALID_ARG, "%s: null corpus", who);
+  if (d.corpus_dtype == HS_FP8_E4M3 && d.n_corpus > 0 && !row_scale)
+    return fail(HS_ERR_INVALID_ARG, "%s: FP8 corpus needs row_scale", who);
+  if (!aligned(q_unique, 16) || !aligned(corpus, 16) || !aligned(row_scale, 4))
+    return fail(HS_ERR_ALIGNMENT, "%s: q_unique/corpus must be 16-byte aligned", who);
+  return check_score_ws(plan, ws, ws_bytes, who);
+}
+
+hs_status hs_score_partial(const hs_plan *plan, const void *q_unique, int64_t n_unique,
+                           const int64_t *n_unique_dev, const void *corpus,
+                           const float *row_scale, void *ws, size_t ws_bytes, void *stream) {
+  if (!plan) return fail(HS_ERR_INVALID_ARG, "hs_score_partial: null plan");
+  hs_status s = check_partial(plan, q_unique, n_unique, n_unique_dev, corpus, row_scale, ws,
+                              ws_bytes, "hs_score_partial");
+  if (s != HS_OK) return s;
+  const hs_merge_desc &d = plan->d;
+  hipError_t e = hs::launch_score_partial(q_unique, corpus, row_scale, d.n_corpus, d.dim, d.k,
+                                          n_unique, n_unique_dev, plan->cap, d.corpus_dtype, ws,
+                                          (hipStream_t)stream);
+  return device_status(e, "hs_score_partial launch");
+}
+
+hs_status hs_topk_merge(const hs_plan *plan, int64_t n_unique, const int64_t *n_unique_dev,
+                        float *topk_score, int32_t *topk_index, void *ws, size_t ws_bytes,
+                        void *stream) {
+  if (!plan) return fail(HS_ERR_INVALID_ARG, "hs_topk_merge: null plan");
+  hs_status s = check_nu(plan, n_unique, n_unique_dev, "hs_topk_merge");
+  if (s != HS_OK) return s;
+  if ((!topk_score || !topk_index) && n_unique != 0)
+    return fail(HS_ERR_INVALID_ARG, "hs_topk_merge: null output");
+  if (!aligned(topk_score, 4) || !aligned(topk_index, 4))
+    return fail(HS_ERR_ALIGNMENT, "hs_topk_merge: misaligned output");
+  s = check_score_ws(plan, ws, ws_bytes, "hs_topk_merge");
+  if (s != HS_OK) return s;
+  const hs_merge_desc &d = plan->d;
+  hipError_t e = hs::launch_topk_merge(ws, n_unique, n_unique_dev, plan->cap, d.n_corpus, d.k,
+                                       d.corpus_dtype, topk_score, topk_index,
+                                       (hipStream_t)stream);
+  return device_status(e, "hs_topk_merge launch");
+}
+
+hs_status hs_score_topk(const hs_plan *plan, const void *q_unique, int64_t n_unique,
+                        const int64_t *n_unique_dev, const void *corpus, const float *row_scale,
+                        float *topk_score, int32_t *topk_index, void *ws, size_t ws_bytes,
+                        void *stream) {
+  if (!plan) return fail(HS_ERR_INVALID_ARG, "hs_score_topk: null plan");
+  hs_status s = check_partial(plan, q_unique, n_unique, n_unique_dev, corpus, row_scale, ws,
+                              ws_bytes, "hs_score_topk");
+  if (s != HS_OK) return s;
+  if ((!topk_score || !topk_index) && n_unique != 0)
+    return fail(HS_ERR_INVALID_ARG, "hs_score_topk: null output");
+  if (!aligned(topk_score, 4) || !aligned(topk_index, 4))
+    return fail(HS_ERR_ALIGNMENT, "hs_score_topk: misaligned output");
+  s = hs_score_partial(plan, q_unique, n_unique, n_unique_dev, corpus, row_scale, ws, ws_bytes,
+                       stream);
+  if (s != HS_OK) return s;
+  return hs_topk_merge(plan, n_unique, n_unique_dev, topk_score, topk_index, ws, ws_bytes,
+                       stream);
+}
+
+hs_status hs_scatter(const void *src, int64_t src_rows, int64_t row_bytes, const void *index,
+                     int32_t index_is_i64, int64_t n_out, const int64_t *n_out_dev, void *dst,
+                     void *stream) {
+  if (src_rows < 0 || n_out < 0)
+    return fail(HS_ERR_INVALID_ARG, "hs_scatter: negative size");
+  if (row_bytes <= 0 || row_bytes % 4 != 0)
+    return fail(HS_ERR_INVALID_ARG, "hs_scatter: row_bytes %lld must be a positive multiple of 4",
+                (long long)row_bytes);
+  if (index_is_i64 != 0 && index_is_i64 != 1)
+    return fail(HS_ERR_INVALID_ARG, "hs_scatter: index_is_i64 must be 0 or 1");
+  if (n_out > 0 && src_rows > 0 && (!src || !index || !dst))
+    return fail(HS_ERR_INVALID_ARG, "hs_scatter: null argument");
+  if (!aligned(src, 4) || !aligned(dst, 4) || !aligned(index, index_is_i64 ? 8 : 4) ||
+      !aligned(n_out_dev, 8))
+    return fail(HS_ERR_ALIGNMENT, "hs_scatter: misaligned pointer");
+  if (n_out == 0 || src_rows == 0) return ok();
+  hipError_t e = hs::launch_gather(src, src_rows, row_bytes, index, index_is_i64, n_out,
+                                   n_out_dev, dst, (hipStream_t)stream);
+  return device_status(e, "hs_scatter launch");
+}
+
+}  // extern "C"

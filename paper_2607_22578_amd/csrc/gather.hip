@@ -1,0 +1,71 @@
+// Steps 2, 2' and 5: row gather dst[i] = src[index[i]].
+//
+// HeraSys Sec. 3.3 (I): the surviving node runs once and its output flows to
+// the downstream nodes of every related query.  Expressed as a gather (each
+// destination row pulls from its source) the delivery has no write conflicts.
+// The same kernel builds the representative query batch (index = survivor of
+// each group) and the embedding rows of distinct chunk ids.
+//
+// A group of G threads copies one row with G consecutive vector accesses
+// (16-byte when the row allows, else 4-byte), so a wavefront reads and writes
+// whole contiguous row segments.
+#include "common.h"
+
+namespace hs {
+
+template <typename V, typename I>
+__global__ __launch_bounds__(256) void gather_rows_kernel(
+    const V *__restrict__ src, int64_t src_rows, int vpr, int group, const I *__restrict__ index,
+    int64_t n_out, const int64_t *__restrict__ n_out_dev, V *__restrict__ dst) {
+  int64_t n = n_out;
+  if (n_out_dev) {
+    int64_t m = *n_out_dev;
+    if (m < n) n = m;
+  }
+  const int rows_per_block = 256 / group;
+  const int sub = threadIdx.x / group, lane = threadIdx.x % group;
+  for (int64_t row = (int64_t)blockIdx.x * rows_per_block + sub; row < n;
+       row += (int64_t)gridDim.x * rows_per_block) {
+    int64_t r = (int64_t)index[row];
+    if (r < 0 || r >= src_rows) continue;
+    const V *s = src + r * vpr;
+    V *d = dst + row * vpr;
+    for (int c = lane; c < vpr; c += group) d[c] = s[c];
+  }
+}
+
+template <typename V>
+static hipError_t launch_gather_t(const void *src, int64_t src_rows, int64_t row_bytes,
+                                  const void *index, int is64, int64_t n_out,
+                                  const int64_t *n_out_dev, void *dst, hipStream_t st) {
+  const int vpr = (int)(row_bytes / (int64_t)sizeof(V));
+  int group = 1;
+  while (group < vpr && group < 256) group <<= 1;
+  const int rows_per_block = 256 / group;
+  int64_t blocks = (n_out + rows_per_block - 1) / rows_per_block;
+  if (blocks > 65536) blocks = 65536;
+  if (blocks < 1) blocks = 1;
+  if (is64)
+    hipLaunchKernelGGL((gather_rows_kernel<V, int64_t>), dim3((unsigned)blocks), dim3(256), 0, st,
+                       (const V *)src, src_rows, vpr, group, (const int64_t *)index, n_out,
+                       n_out_dev, (V *)dst);
+  else
+    hipLaunchKernelGGL((gather_rows_kernel<V, int32_t>), dim3((unsigned)blocks), dim3(256), 0, st,
+                       (const V *)src, src_rows, vpr, group, (const int32_t *)index, n_out,
+                       n_out_dev, (V *)dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const void *src, int64_t src_rows, int64_t row_bytes, const void *index,
+                         int is64, int64_t n_out, const int64_t *n_out_dev, void *dst,
+                         hipStream_t st) {
+  if (n_out <= 0) return hipSuccess;
+  bool v16 = (row_bytes % 16 == 0) && (((uintptr_t)src | (uintptr_t)dst) % 16 == 0);
+  if (v16)
+    return launch_gather_t<uint4>(src, src_rows, row_bytes, index, is64, n_out, n_out_dev, dst,
+                                  st);
+  return launch_gather_t<uint32_t>(src, src_rows, row_bytes, index, is64, n_out, n_out_dev, dst,
+                                   st);
+}
+
+}  // namespace hs

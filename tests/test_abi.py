@@ -1,0 +1,132 @@
+"""The C ABI: the library loads, exports every declared symbol, and rejects bad
+arguments on the host before any HIP call (so these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_22578_amd as hs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    txt = open(os.path.join(ROOT, "include", "hs_merge.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(hs_[a-z_]+)\s*\(", txt)))
+
+
+def test_exports_every_declared_symbol():
+    decl = _declared()
+    assert set(decl) == set(hs.EXPORTS), decl
+    lib = ctypes.CDLL(hs.LIB_PATH)
+    for name in decl:
+        assert hasattr(lib, name), name
+
+
+def test_abi_version_and_status_strings():
+    assert hs.hs_abi_version() == hs.ABI_VERSION == 1
+    assert hs.hs_status_string(hs.HS_OK) == "HS_OK"
+    assert hs.hs_status_string(hs.HS_ERR_WORKSPACE) == "HS_ERR_WORKSPACE"
+    assert hs.hs_status_string(99) == "HS_ERR_UNKNOWN"
+
+
+GOOD = dict(n_requests=2048, dim=768, n_corpus=1_000_000, k=10, query_dtype=hs.HS_BF16,
+            corpus_dtype=hs.HS_BF16)
+
+
+def test_plan_ok_and_workspace():
+    p = hs.hs_merge_plan(**GOOD)
+    assert p.workspace_bytes > 0
+    p2 = hs.hs_merge_plan(**dict(GOOD, n_requests=262_144, k=10))
+    assert p2.workspace_bytes >= 262_144 * 24   # radix dedup buffers
+    p3 = hs.hs_merge_plan(**dict(GOOD, n_requests=0))
+    assert p3.workspace_bytes >= 0
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(k=0), hs.HS_ERR_INVALID_ARG),
+    (dict(k=1025), hs.HS_ERR_INVALID_ARG),
+    (dict(dim=0), hs.HS_ERR_INVALID_ARG),
+    (dict(dim=20000), hs.HS_ERR_INVALID_ARG),
+    (dict(dim=764), hs.HS_ERR_UNSUPPORTED),                      # bf16 needs d % 8
+    (dict(dim=776, corpus_dtype=hs.HS_FP8_E4M3), hs.HS_ERR_UNSUPPORTED),  # fp8 needs d % 16
+    (dict(n_requests=-1), hs.HS_ERR_INVALID_ARG),
+    (dict(n_requests=2 ** 31), hs.HS_ERR_INVALID_ARG),
+    (dict(n_corpus=-5), hs.HS_ERR_INVALID_ARG),
+    (dict(n_corpus=2 ** 31), hs.HS_ERR_INVALID_ARG),
+    (dict(query_dtype=7), hs.HS_ERR_UNSUPPORTED),
+    (dict(query_dtype=hs.HS_F32), hs.HS_ERR_UNSUPPORTED),         # f32 queries + bf16 corpus
+    (dict(corpus_dtype=hs.HS_F32), hs.HS_ERR_UNSUPPORTED),        # bf16 queries + f32 corpus
+    (dict(max_unique=5000), hs.HS_ERR_INVALID_ARG),
+    (dict(flags=1), hs.HS_ERR_INVALID_ARG),
+])
+def test_plan_rejects(bad, code):
+    with pytest.raises(hs.HsError) as e:
+        hs.hs_merge_plan(**dict(GOOD, **bad))
+    assert e.value.status == code
+    assert hs.hs_last_error()
+
+
+FAKE = 0x10000000   # never dereferenced: validation fails first
+
+
+def test_dedup_validation():
+    p = hs.hs_merge_plan(**dict(GOOD, n_requests=100_000))
+    with pytest.raises(hs.HsError) as e:   # no workspace
+        hs.hs_dedup(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0)
+    assert e.value.status == hs.HS_ERR_WORKSPACE
+    with pytest.raises(hs.HsError) as e:   # workspace too small
+        hs.hs_dedup(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 1000)
+    assert e.value.status == hs.HS_ERR_WORKSPACE
+    with pytest.raises(hs.HsError) as e:   # misaligned keys
+        hs.hs_dedup(p, FAKE + 4, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, p.workspace_bytes)
+    assert e.value.status == hs.HS_ERR_ALIGNMENT
+    with pytest.raises(hs.HsError) as e:   # null output
+        hs.hs_dedup(p, FAKE, None, FAKE, FAKE, FAKE, FAKE, None, FAKE, p.workspace_bytes)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    with pytest.raises(hs.HsError) as e:   # misaligned workspace
+        hs.hs_dedup(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE + 16, p.workspace_bytes)
+    assert e.value.status == hs.HS_ERR_ALIGNMENT
+
+
+def test_score_validation():
+    p = hs.hs_merge_plan(**GOOD)
+    ws = p.workspace_bytes
+    with pytest.raises(hs.HsError) as e:   # n_unique beyond the plan
+        hs.hs_score_topk(p, FAKE, 4096, None, FAKE, None, FAKE, FAKE, FAKE, ws)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    with pytest.raises(hs.HsError) as e:   # -1 without device count
+        hs.hs_score_topk(p, FAKE, -1, None, FAKE, None, FAKE, FAKE, FAKE, ws)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    with pytest.raises(hs.HsError) as e:   # misaligned corpus
+        hs.hs_score_topk(p, FAKE, 10, None, FAKE + 2, None, FAKE, FAKE, FAKE, ws)
+    assert e.value.status == hs.HS_ERR_ALIGNMENT
+    with pytest.raises(hs.HsError) as e:   # workspace too small
+        hs.hs_score_partial(p, FAKE, 10, None, FAKE, None, FAKE, ws - 1)
+    assert e.value.status == hs.HS_ERR_WORKSPACE
+    with pytest.raises(hs.HsError) as e:
+        hs.hs_topk_merge(p, 10, None, None, FAKE, FAKE, ws)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    p8 = hs.hs_merge_plan(**dict(GOOD, corpus_dtype=hs.HS_FP8_E4M3))
+    with pytest.raises(hs.HsError) as e:   # fp8 without row scale
+        hs.hs_score_topk(p8, FAKE, 10, None, FAKE, None, FAKE, FAKE, FAKE, p8.workspace_bytes)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+
+
+def test_scatter_validation():
+    with pytest.raises(hs.HsError) as e:
+        hs.hs_scatter(FAKE, 10, 6, FAKE, 0, 5, None, FAKE)      # row_bytes % 4
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    with pytest.raises(hs.HsError) as e:
+        hs.hs_scatter(FAKE, 10, 8, FAKE, 2, 5, None, FAKE)      # bad index flag
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    with pytest.raises(hs.HsError) as e:
+        hs.hs_scatter(FAKE, 10, 8, FAKE + 4, 1, 5, None, FAKE)  # misaligned i64 index
+    assert e.value.status == hs.HS_ERR_ALIGNMENT
+    with pytest.raises(hs.HsError) as e:
+        hs.hs_scatter(None, 10, 8, FAKE, 0, 5, None, FAKE)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    # empty work is a no-op that never touches the device
+    hs.hs_scatter(FAKE, 10, 8, FAKE, 0, 0, None, FAKE)

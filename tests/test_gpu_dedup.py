@@ -1,0 +1,100 @@
+"""Dedup on the GPU, bit-exact against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from gpu_harness import device, note
+
+pytestmark = pytest.mark.gpu
+
+I64_MIN = np.iinfo(np.int64).min
+I64_MAX = np.iinfo(np.int64).max
+
+
+def _gpu_dedup(keys, host_count=False):
+    import paper_2607_22578_amd as hs
+    import oracle
+    dev = device()
+    R = keys.shape[0]
+    plan = hs.hs_merge_plan(R, 8, 1, 1, hs.HS_BF16, hs.HS_BF16)
+    ws = torch.empty(max(plan.workspace_bytes, 256), dtype=torch.uint8, device=dev)
+    R1 = max(R, 1)
+    kd = torch.from_numpy(keys.astype(np.int64)).to(dev) if R else None
+    uk = torch.full((R1,), 7, dtype=torch.int64, device=dev)
+    fi = torch.full((R1,), -7, dtype=torch.int32, device=dev)
+    ct = torch.full((R1,), -7, dtype=torch.int32, device=dev)
+    inv = torch.full((R1,), -7, dtype=torch.int32, device=dev)
+    nu = torch.full((1,), -7, dtype=torch.int64, device=dev)
+    st = torch.cuda.current_stream(dev)
+    nh = hs.hs_dedup(plan, kd, uk, fi, ct, inv, nu, True if host_count else None, ws, stream=st)
+    torch.cuda.synchronize(dev)
+    ref = oracle.dedup(keys)
+    n = int(nu.item())
+    assert n == ref["n_unique"]
+    if host_count:
+        assert nh == n
+    np.testing.assert_array_equal(uk[:n].cpu().numpy(), ref["unique_keys"])
+    np.testing.assert_array_equal(fi[:n].cpu().numpy(), ref["first_index"])
+    np.testing.assert_array_equal(ct[:n].cpu().numpy(), ref["counts"])
+    np.testing.assert_array_equal(inv[:R].cpu().numpy(), ref["inverse"])
+    return uk[:n].cpu().numpy(), inv[:R].cpu().numpy()
+
+
+@pytest.mark.parametrize("name", ["tiny", "ridge1m", "mfma4m", "fp8_20m", "dedup256k"])
+def test_dedup_workload_keys(name):
+    w = synth.make(name, with_corpus=False)
+    note(f"dedup {name} R={w.R}")
+    _gpu_dedup(w.keys, host_count=(name == "ridge1m"))
+
+
+@pytest.mark.parametrize("case", ["one", "two_equal", "all_equal_small", "all_equal_radix",
+                                  "distinct_small", "distinct_radix", "extremes_small",
+                                  "extremes_radix", "negative", "boundary_4096",
+                                  "boundary_4097", "ragged_radix", "narrow_range_radix",
+                                  "wide_and_narrow"])
+def test_dedup_edge_cases(case):
+    rng = np.random.default_rng(abs(hash(case)) % (2 ** 32))
+    if case == "one":
+        keys = np.array([12345], np.int64)
+    elif case == "two_equal":
+        keys = np.array([-3, -3], np.int64)
+    elif case == "all_equal_small":
+        keys = np.full(3000, I64_MIN, np.int64)
+    elif case == "all_equal_radix":
+        keys = np.full(50_000, 42, np.int64)
+    elif case == "distinct_small":
+        keys = rng.permutation(4000).astype(np.int64) * 7919 - 10 ** 6
+    elif case == "distinct_radix":
+        keys = rng.integers(I64_MIN, I64_MAX, size=70_000, dtype=np.int64, endpoint=True)
+    elif case == "extremes_small":
+        keys = rng.choice(np.array([I64_MIN, I64_MAX, 0, -1, 1], np.int64), size=1000)
+    elif case == "extremes_radix":
+        keys = rng.choice(np.array([I64_MIN, I64_MAX, 0, -1, 1, I64_MIN + 1], np.int64),
+                          size=9000)
+    elif case == "negative":
+        keys = -rng.integers(1, 500, size=6000).astype(np.int64)
+    elif case == "boundary_4096":
+        keys = rng.integers(0, 1000, size=4096).astype(np.int64)
+    elif case == "boundary_4097":
+        keys = rng.integers(0, 1000, size=4097).astype(np.int64)
+    elif case == "ragged_radix":
+        keys = rng.integers(-2 ** 40, 2 ** 40, size=3 * 4096 + 77).astype(np.int64)
+    elif case == "narrow_range_radix":        # 18-bit span, far from zero
+        keys = (rng.integers(0, 200_000, size=100_000) + 2 ** 50).astype(np.int64)
+    else:                                     # one outlier forces all 64 bits
+        keys = rng.integers(0, 300, size=20_000).astype(np.int64)
+        keys[12345] = I64_MIN
+    _gpu_dedup(keys)
+
+
+def test_dedup_empty():
+    _gpu_dedup(np.zeros(0, np.int64))
+
+
+def test_dedup_deterministic():
+    w = synth.make("mfma4m", with_corpus=False)
+    a = _gpu_dedup(w.keys)
+    b = _gpu_dedup(w.keys)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
