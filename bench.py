@@ -1,0 +1,240 @@
+#!/usr/bin/env python3
+"""Benchmark of the merged-retrieval hot path on one MI355X.
+
+One step = one merge window of the whole path on the device: dedup of the
+request signatures, gather of the representative query rows, exact bf16 MFMA
+scoring + top-k of the distinct queries against the HBM-resident corpus, and
+delivery of every result to each request.  Inputs are synthetic (seeded) and
+resident in HBM before timing starts; the distinct count stays on the device
+(no host synchronisation inside a step).
+
+Default workload: 64 workflows x 32 retrieval queries, query ids Zipf(1.1)
+over 512 templates, d=768 bf16 unit-norm, 1,000,000-chunk bf16 corpus, k=10.
+
+Prints ONE JSON line.  `value` = logical requests per second of the timed
+steps.  `roofline` describes the dominant kernel (the scoring kernel), timed
+with HIP events on its own stream inside the timed region.  `cpu_baseline`
+times the CPU oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "merged retrieval queries/s + achieved HBM GB/s or MFMA % (dedup+score+top-k)"
+PEAK_HBM_GBS = 8000.0
+PEAK_MFMA = {"bf16": 2500.0}          # dense TFLOP/s (no sparsity)
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_partial_ridge1m_traffic.json")
+KERNEL_SOURCES = ["paper_2607_22578_amd/csrc/score.hip", "paper_2607_22578_amd/csrc/common.h"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="ridge1m",
+                    help="ridge1m (default), mfma4m or fp8_20m")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=48,
+                    help="distinct queries scored by the oracle for the CPU baseline")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="only run a plain device copy of this many bytes (counter calibration)")
+    return ap.parse_args()
+
+
+def copy_calibration(nbytes: int):
+    import torch
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "launches": 5}), flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU; the multi-GPU (corpus-sharded) path is a "
+              "design only, so --gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_bytes:
+        copy_calibration(args.copy_bytes)
+        return
+
+    import numpy as np
+    import torch
+
+    import paper_2607_22578_amd as hs
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t_gen = time.time()
+    w = synth.make(args.workload)
+    t_gen = time.time() - t_gen
+    cfg = w.cfg
+    R, d, N, k = w.R, w.dim, w.n_corpus, w.k
+    qdt = hs.HS_BF16
+    cdt = {"bf16": hs.HS_BF16, "fp8": hs.HS_FP8_E4M3}[cfg.c_enc]
+
+    def to_dev(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    keys, q_req, corpus = to_dev(w.keys), to_dev(w.q_req), to_dev(w.corpus)
+    scale = to_dev(w.scale) if w.scale is not None else None
+    m = hs.MergedRetrieval(R, d, N, k, qdt, cdt, device=dev)
+    stream = torch.cuda.Stream(dev)   # default priority
+
+    def step(ev=None):
+        m.dedup(keys, stream)
+        m.gather_queries(q_req, stream)
+        if ev is not None:
+            ev[0].record(stream)
+        m.score_partial(corpus, scale, -1, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        m.topk_merge(-1, stream)
+        m.deliver(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+    n_u = int(m.n_unique.item())
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize(dev)
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    t_end.record(stream)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - wall0
+    total_ms = t_start.elapsed_time(t_end)
+    ms_per_step = total_ms / args.steps
+    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+
+    # stage breakdown (separate, untimed-for-value pass)
+    st_ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    reps = 10
+    acc = np.zeros(5)
+    for _ in range(reps):
+        st_ev[0].record(stream)
+        m.dedup(keys, stream)
+        st_ev[1].record(stream)
+        m.gather_queries(q_req, stream)
+        st_ev[2].record(stream)
+        m.score_partial(corpus, scale, -1, stream)
+        st_ev[3].record(stream)
+        m.topk_merge(-1, stream)
+        st_ev[4].record(stream)
+        m.deliver(stream)
+        st_ev[5].record(stream)
+        torch.cuda.synchronize(dev)
+        acc += [st_ev[i].elapsed_time(st_ev[i + 1]) for i in range(5)]
+    stages = dict(zip(["dedup", "gather", "score_partial", "topk_merge", "deliver"],
+                      (acc / reps).round(4).tolist()))
+
+    # roofline of the scoring kernel: algorithmic work per launch
+    c_bytes = N * d * (1 if cfg.c_enc == "fp8" else 2) + (N * 4 if cfg.c_enc == "fp8" else 0)
+    q_bytes = n_u * d * 2
+    alg_bytes = c_bytes + q_bytes
+    alg_flops = 2.0 * n_u * N * d
+    t_s = kern_ms * 1e-3
+    tflops = alg_flops / t_s / 1e12
+    gbs = alg_bytes / t_s / 1e9
+    t_mfma = alg_flops / (PEAK_MFMA["bf16"] * 1e12)
+    t_hbm = alg_bytes / (PEAK_HBM_GBS * 1e9)
+    if t_mfma >= t_hbm:
+        roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_MFMA["bf16"],
+                "unit": "TFLOP/s", "frac": round(tflops / PEAK_MFMA["bf16"], 4)}
+    else:
+        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    roof["traffic"] = None
+    roof["kernel"] = "score_partial_mfma"
+    roof["kernel_ms"] = round(kern_ms, 4)
+    roof["algorithmic_bytes"] = alg_bytes
+    roof["algorithmic_flops"] = alg_flops
+    roof["hbm_gbs_algorithmic"] = round(gbs, 1)
+    roof["hbm_frac_algorithmic"] = round(gbs / PEAK_HBM_GBS, 4)
+    roof["mfma_frac"] = round(tflops / PEAK_MFMA["bf16"], 4)
+    src_hash = kernel_source_hash()
+    roof["kernel_source"] = src_hash
+    if args.workload == "ridge1m" and os.path.exists(TRAFFIC_FILE):
+        tr = json.load(open(TRAFFIC_FILE))
+        if tr.get("kernel_source") == src_hash:
+            roof["traffic"] = tr.get("hbm_bytes_per_launch")
+
+    value = R * args.steps / (total_ms * 1e-3)
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "queries/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.desc}", "n_requests": R, "n_unique": n_u,
+                   "dim": d, "n_corpus": N, "k": k, "query_dtype": cfg.q_enc,
+                   "corpus_dtype": cfg.c_enc, "seed": w.seed},
+        "unique_queries_per_s": round(n_u * args.steps / (total_ms * 1e-3), 1),
+        "stages_ms": stages,
+        "wall_s_timed": round(wall, 4),
+        "roofline": roof,
+    }
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, n_u, args.cpu_sample)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, n_u: int, n_sample: int) -> dict:
+    """The oracle on the host: full dedup and representative gather, exact
+    scoring + top-k for a seeded sample of distinct queries over the whole
+    corpus, extrapolated to all n_u distinct queries."""
+    import numpy as np
+
+    import oracle
+    threads = oracle.default_threads()
+    t0 = time.perf_counter()
+    ref = oracle.dedup(w.keys)
+    rows = oracle.gather_rows(w.q_req, ref["first_index"])
+    t_dedup = time.perf_counter() - t0
+    rng = np.random.default_rng(1)
+    n_sample = min(n_sample, ref["n_unique"])
+    sel = np.sort(rng.choice(ref["n_unique"], size=n_sample, replace=False))
+    t1 = time.perf_counter()
+    oracle.topk_exact(rows, w.corpus, w.k, scale=w.scale, q_rows=sel, threads=threads)
+    t_score = time.perf_counter() - t1
+    t_full = t_dedup + t_score * ref["n_unique"] / n_sample
+    return {"value": round(w.R / t_full, 2), "unit": "queries/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"dedup+gather of all {w.R} requests, exact fp64 top-{w.k} of "
+                      f"{n_sample}/{ref['n_unique']} distinct queries over all {w.n_corpus} "
+                      f"rows ({t_score:.1f} s), extrapolated to all distinct queries",
+            "measured_s": round(t_dedup + t_score, 2)}
+
+
+if __name__ == "__main__":
+    main()

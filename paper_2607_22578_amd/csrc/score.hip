@@ -33,18 +33,12 @@ namespace hs {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 constexpr int kMaxSK = 8192;        // bound on S*k (merge list length per query)
 constexpr int kListLdsMaxK = 32;    // slice lists live in LDS up to this k
 constexpr int kGridMax = 512;       // persistent grid never exceeds this
-
-// MFMA path tiles
-constexpr int kMQ = 128;            // queries per tile
-constexpr int kNC = 128;            // corpus rows per tile
-constexpr int kKC = 64;             // K per LDS stage
-constexpr int kLda = kKC + 8;       // staged row stride (bf16 elements)
-constexpr int kDumpLd = kNC + 4;    // dumped scores: floats per query row
 
 // VALU (fp32) path tiles
 constexpr int kVMQ = 64;
@@ -167,6 +161,71 @@ __device__ void flush_lists(const TileState &ts, const ScoreArgs &a, int64_t qba
 }
 
 // ---------------------------------------------------------------- MFMA path
+//
+// Workgroup = 4 waves (one per SIMD).  Tile = 256 corpus rows x MQ = 16*QB
+// queries; wave w owns rows [64w, 64w+64) of the tile for all MQ queries, as
+// 4 x QB MFMA 16x16x32 blocks (A = 16 corpus rows, B = 16 queries, fp32 C).
+//
+// Operand paths, per K chunk of 64:
+//   corpus: global -> registers directly (each wave loads only its own rows,
+//           so nothing is shared and no LDS is needed), one chunk ahead;
+//   queries: global -> registers -> a 3-slot LDS ring (two chunks ahead),
+//           XOR-swizzled by row so that fragment reads are conflict-free.
+// Only the query operand is read from LDS: 64 corpus rows reuse each query
+// fragment, which keeps LDS traffic near half of its bandwidth at full MFMA
+// rate.  Inside an MFMA the K order is free as long as A and B agree, so each
+// lane takes the k-slice of a chunk that makes its corpus loads contiguous.
+//
+// Top-k epilogue, per tile and query: each lane holds 16 scores of each of
+// its QB queries (4 rows of each row block).  It compares their maximum with
+// the query's running threshold (registers); only on a hit are single scores
+// appended to a small per-query LDS queue, which one thread per query then
+// merges into the query's k-list (replace-the-minimum).  A full queue stops
+// the lane at that score; it resumes there after the merge has raised the
+// threshold, so no candidate is lost and none is seen twice.  Before the
+// first tile of a work item is filtered, the threshold is seeded with the
+// smallest of at least k group maxima of that tile (the 16 lanes holding a
+// query each split their rows into groups): those maxima are k distinct
+// scores, so their minimum never exceeds the true k-th best score.
+
+constexpr int kW2 = 4;                      // waves per workgroup (one per SIMD)
+constexpr int kT2 = kW2 * 64;               // threads per workgroup
+constexpr int kRB = 4;                      // 16-row blocks per wave
+constexpr int kNC2 = kW2 * 16 * kRB;        // 256 rows per tile
+constexpr int kKC2 = 64;                    // K per chunk
+constexpr int kQcap = 16;                   // queue slots per query
+constexpr int kLanesQ = kW2 * 4;            // lanes holding one query in a tile
+constexpr int kQB = 7;                      // query blocks of 16 per tile
+constexpr int kMQ2 = 16 * kQB;              // 112 queries per tile
+constexpr int kRing = 2;                    // corpus chunks held in registers
+
+struct Lds2 {
+  uint16_t *bring;   // [3][MQ][64] bf16, swizzled
+  uint64_t *queue;   // [MQ][kQcap]
+  float *gm;         // [MQ][kLanesQ * kRB] warm-up group maxima
+  int32_t *qcount;   // [MQ]
+  float *thr0;       // [MQ]
+  float *sscale;     // [kNC2]
+  int32_t *flags;    // [0] hit epoch, [1] overflow epoch
+  float *stash;      // [threads][4 * kRB] scores of one query block (rare path)
+  TileState ts;
+};
+
+// Warm-up groups per lane and query: the rows a lane holds for one query
+// are cut into gpl groups so that kLanesQ * gpl >= k group maxima exist; the
+// smallest of them is a valid lower bound for the k-th best score.  0 = no
+// warm-up (k too large).
+__host__ __device__ constexpr int warm_groups(int k) {
+  int g = 1;
+  while (g <= kRB && kLanesQ * g < k) g <<= 1;
+  return g <= kRB ? g : 0;
+}
+
+__host__ __device__ constexpr int mfma2_lds_bytes(bool lds_lists, int k) {
+  return 3 * kMQ2 * kKC2 * 2 + kMQ2 * kQcap * 8 + kMQ2 * 4 + kMQ2 * 4 + kNC2 * 4 + 16 +
+         kT2 * kRB * 4 * 4 + kMQ2 * kLanesQ * kRB * 4 + kMQ2 * (8 + 4 + 4 + 4) +
+         (lds_lists ? kMQ2 * k * 8 : 0);
+}
 
 __device__ __forceinline__ void cvt_fp8x4_to_bf16(uint32_t w, uint32_t &lo, uint32_t &hi) {
   // exact e4m3 -> bf16 (every e4m3 value is representable in bf16)
@@ -176,219 +235,461 @@ __device__ __forceinline__ void cvt_fp8x4_to_bf16(uint32_t w, uint32_t &lo, uint
   hi = __builtin_bit_cast(uint32_t, b);
 }
 
+__device__ __forceinline__ bf16x8 fp8x8_to_bf16(uint32_t lo, uint32_t hi) {
+  uint32_t o0, o1, o2, o3;
+  cvt_fp8x4_to_bf16(lo, o0, o1);
+  cvt_fp8x4_to_bf16(hi, o2, o3);
+  uint4 v = make_uint4(o0, o1, o2, o3);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// piece (16 bytes = 8 bf16) of a 64-wide K chunk that lane group g feeds to
+// MFMA step s: bf16 corpus rows are loaded as two contiguous 64-byte halves,
+// fp8 rows as one 16-byte slice per lane group
 template <bool FP8>
-struct StageRegs {
-  uint4 a[FP8 ? 2 : 4];
-  uint4 b[4];
+__device__ __forceinline__ int kpiece(int g, int s) {
+  return FP8 ? 2 * g + s : g + 4 * s;
+}
+
+__device__ __forceinline__ int swz(int q, int p) { return q * 64 + ((p ^ (q & 7)) << 3); }
+
+// Per-item state of the top-k epilogue.
+struct EpiState {
+  int qbase, qvalid, s_;
+  int64_t S;
+  int epoch;
 };
 
-// Load one K stage of the corpus tile (rows rbase..+NC) and query tile
-// (qbase..+MQ) from global memory; out-of-range rows/columns read as zero.
-template <bool FP8>
-__device__ __forceinline__ void stage_load(StageRegs<FP8> &r, const ScoreArgs &a, int64_t rbase,
-                                           int64_t qbase, int64_t nu, int kc) {
-  const int tid = threadIdx.x;
-  if constexpr (FP8) {
-    const uint8_t *C = (const uint8_t *)a.corpus;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      int c = tid + kThreads * i;
-      int row = c >> 2, c16 = c & 3;
-      int64_t gr = rbase + row;
-      int col = kc + c16 * 16;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (gr < a.N && col < a.d) v = *reinterpret_cast<const uint4 *>(C + gr * a.d + col);
-      r.a[i] = v;
-    }
-  } else {
-    const uint16_t *C = (const uint16_t *)a.corpus;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int c = tid + kThreads * i;
-      int row = c >> 3, c8 = c & 7;
-      int64_t gr = rbase + row;
-      int col = kc + c8 * 8;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (gr < a.N && col < a.d) v = *reinterpret_cast<const uint4 *>(C + gr * a.d + col);
-      r.a[i] = v;
-    }
-  }
-  const uint16_t *Q = (const uint16_t *)a.q;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int c = tid + kThreads * i;
-    int row = c >> 3, c8 = c & 7;
-    int64_t gq = qbase + row;
-    int col = kc + c8 * 8;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (gq < nu && col < a.d) v = *reinterpret_cast<const uint4 *>(Q + gq * a.d + col);
-    r.b[i] = v;
-  }
-}
-
-template <bool FP8>
-__device__ __forceinline__ void stage_store(const StageRegs<FP8> &r, uint16_t *As, uint16_t *Bs) {
-  const int tid = threadIdx.x;
-  if constexpr (FP8) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      int c = tid + kThreads * i;
-      int row = c >> 2, c16 = c & 3;
-      uint4 v = r.a[i];
-      uint4 o0, o1;
-      cvt_fp8x4_to_bf16(v.x, o0.x, o0.y);
-      cvt_fp8x4_to_bf16(v.y, o0.z, o0.w);
-      cvt_fp8x4_to_bf16(v.z, o1.x, o1.y);
-      cvt_fp8x4_to_bf16(v.w, o1.z, o1.w);
-      uint16_t *dst = As + row * kLda + c16 * 16;
-      *reinterpret_cast<uint4 *>(dst) = o0;
-      *reinterpret_cast<uint4 *>(dst + 8) = o1;
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int c = tid + kThreads * i;
-      int row = c >> 3, c8 = c & 7;
-      *reinterpret_cast<uint4 *>(As + row * kLda + c8 * 8) = r.a[i];
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int c = tid + kThreads * i;
-    int row = c >> 3, c8 = c & 7;
-    *reinterpret_cast<uint4 *>(Bs + row * kLda + c8 * 8) = r.b[i];
-  }
-}
-
-constexpr int kStageBytes = (kNC + kMQ) * kLda * 2;           // one buffer (A + B)
-constexpr int kDumpBytes = kMQ * kDumpLd * 4;
-constexpr int kMfmaFixed = (2 * kStageBytes > kDumpBytes ? 2 * kStageBytes : kDumpBytes);
-constexpr int kSmallBytes = kMQ * (8 + 4 + 4 + 4) + kNC * 4;
-
-__host__ __device__ constexpr int mfma_lds_bytes(bool lds_lists, int k) {
-  return kMfmaFixed + kSmallBytes + (lds_lists ? kMQ * k * 8 : 0);
-}
-
-// 4 waves as 2 (corpus rows) x 2 (queries); each wave owns a 64 x 64 block of
-// scores = 2 x 2 MFMA 32x32 tiles.  MFMA operand A = corpus rows (M), B =
-// queries (N), so each lane's accumulators all belong to the same query
-// column: one running threshold per lane and query block.
+// Top-k epilogue of one corpus tile.  `row0` is the corpus row of the tile's
+// first loaded row; rows below `rlo` (already scored by the previous tile)
+// and at or above N are excluded.
 template <bool FP8, bool LDS_LISTS>
-__global__ __launch_bounds__(kThreads, 1) void score_partial_mfma(ScoreArgs a) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  uint16_t *stage = reinterpret_cast<uint16_t *>(smem);
-  float *dump = reinterpret_cast<float *>(smem);
-  unsigned char *p = smem + kMfmaFixed;
-  TileState ts;
-  ts.lmin = reinterpret_cast<uint64_t *>(p); p += kMQ * 8;
-  ts.lpos = reinterpret_cast<int32_t *>(p); p += kMQ * 4;
-  ts.thr = reinterpret_cast<float *>(p); p += kMQ * 4;
-  ts.flag = reinterpret_cast<int32_t *>(p); p += kMQ * 4;
-  float *sscale = reinterpret_cast<float *>(p); p += kNC * 4;
-  ts.lists = LDS_LISTS ? reinterpret_cast<uint64_t *>(p) : nullptr;
-
-  const int64_t nu = read_nu(a.n_unique, a.n_unique_dev, a.cap);
-  const Split sp = split_for(nu, a.N, kMQ, kNC, a.grid, a.k);
-  const int64_t items = sp.qtiles * sp.S;
+__device__ __forceinline__ void tile_epilogue(const Lds2 &L, const ScoreArgs &a,
+                                              f32x4 (&acc)[kRB][kQB], float (&thr_r)[kQB],
+                                              EpiState &es, int row0, int rlo, bool first) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int wr = wv & 1, wq = wv >> 1;
-  const int nst = (int)((a.d + kKC - 1) / kKC);
-
-  for (int64_t w = logical_wg(a.grid); w < items; w += a.grid) {
-    const int64_t qt = w % sp.qtiles, s = w / sp.qtiles;
-    const int64_t t0 = s * sp.ntiles / sp.S, t1 = (s + 1) * sp.ntiles / sp.S;
-    const int64_t qbase = qt * kMQ;
-    init_lists<kMQ>(ts, a, qbase, nu, sp.S, s);
-    __syncthreads();
-    float tq0 = -__builtin_inff(), tq1 = -__builtin_inff();
-
-    for (int64_t t = t0; t < t1; ++t) {
-      const int64_t rbase = t * kNC;
-      if (FP8 && tid < kNC) sscale[tid] = (rbase + tid < a.N) ? a.scale[rbase + tid] : 0.0f;
-      f32x16 acc[2][2];
+  const int cq = lane & 15, lg = lane >> 4;
+  const int N = (int)a.N;
+  const float ninf = -__builtin_inff();
+  const int rbase = row0 + wv * (16 * kRB) + 4 * lg;   // + 16*rb + j
+  if (FP8) {
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+    for (int rb = 0; rb < kRB; ++rb) {
+      const float4 sc =
+          *reinterpret_cast<const float4 *>(L.sscale + wv * (16 * kRB) + rb * 16 + 4 * lg);
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
-
-      StageRegs<FP8> regs;
-      stage_load<FP8>(regs, a, rbase, qbase, nu, 0);
-      stage_store<FP8>(regs, stage, stage + kNC * kLda);
-      __syncthreads();
-      for (int st = 0; st < nst; ++st) {
-        uint16_t *As = stage + (st & 1) * (kStageBytes / 2);
-        uint16_t *Bs = As + kNC * kLda;
-        if (st + 1 < nst) stage_load<FP8>(regs, a, rbase, qbase, nu, (st + 1) * kKC);
-        const uint16_t *pa = As + (wr * 64 + (lane & 31)) * kLda + (lane >> 5) * 8;
-        const uint16_t *pb = Bs + (wq * 64 + (lane & 31)) * kLda + (lane >> 5) * 8;
-#pragma unroll
-        for (int kk = 0; kk < kKC; kk += 16) {
-          bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(pa + kk);
-          bf16x8 a1 = *reinterpret_cast<const bf16x8 *>(pa + 32 * kLda + kk);
-          bf16x8 b0 = *reinterpret_cast<const bf16x8 *>(pb + kk);
-          bf16x8 b1 = *reinterpret_cast<const bf16x8 *>(pb + 32 * kLda + kk);
-          acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, acc[0][0], 0, 0, 0);
-          acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, acc[0][1], 0, 0, 0);
-          acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
-          acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
-        }
-        if (st + 1 < nst) {
-          uint16_t *An = stage + ((st + 1) & 1) * (kStageBytes / 2);
-          stage_store<FP8>(regs, An, An + kNC * kLda);
-        }
-        __syncthreads();
+      for (int qb = 0; qb < kQB; ++qb) {
+        acc[rb][qb][0] *= sc.x;
+        acc[rb][qb][1] *= sc.y;
+        acc[rb][qb][2] *= sc.z;
+        acc[rb][qb][3] *= sc.w;
       }
+    }
+  }
+  // excluded rows never compete: NaN fails every >= test and is ignored by
+  // fmaxf
+  if (rlo > row0 || row0 + kNC2 > N) {
+#pragma unroll
+    for (int rb = 0; rb < kRB; ++rb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = rbase + rb * 16 + j;
+        if (r >= N || r < rlo)
+#pragma unroll
+          for (int qb = 0; qb < kQB; ++qb) acc[rb][qb][j] = __builtin_nanf("");
+      }
+  }
+  const int gpl = warm_groups(a.k);
+  if (first && gpl > 0) {
+    // warm-up threshold: the smallest of kLanesQ * gpl group maxima
+    const int span = kRB / gpl;   // row blocks per group
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb) {
+      float *dst = L.gm + (qb * 16 + cq) * (kLanesQ * kRB) + (wv * 4 + lg) * gpl;
+      float m = ninf;
+#pragma unroll
+      for (int rb = 0; rb < kRB; ++rb) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) m = fmaxf(m, acc[rb][qb][j]);
+        if ((rb + 1) % span == 0) {
+          dst[rb / span] = m;
+          m = ninf;
+        }
+      }
+    }
+    __syncthreads();
+    if (tid < es.qvalid) {
+      const float *v = L.gm + tid * (kLanesQ * kRB);
+      const int n = kLanesQ * gpl;
+      float mn = v[0];
+      for (int i = 1; i < n; ++i) mn = fminf(mn, v[i]);
+      L.thr0[tid] = mn;
+      L.ts.thr[tid] = mn;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb) thr_r[qb] = L.ts.thr[qb * 16 + cq];
+  }
 
-      // epilogue: lane owns query column (lane & 31) of each query block and
-      // rows 8*(e/4) + 4*(lane/32) + (e%4) of each 32-row block
-      const int rsub = 4 * (lane >> 5);
-      if (FP8) {
+  // candidate rounds: scores at or above the query threshold go to the
+  // query's LDS queue; when a queue is full the remaining bits stay pending
+  uint32_t pending[kQB];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+  for (int qb = 0; qb < kQB; ++qb) pending[qb] = 0;
+  for (int round = 0;; ++round) {
+    bool any = false;
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            float4 sc = *reinterpret_cast<const float4 *>(sscale + wr * 64 + i * 32 + 8 * g + rsub);
+    for (int qb = 0; qb < kQB; ++qb) {
+      const int ql = qb * 16 + cq;
+      const float th = thr_r[qb];
+      uint32_t mask = 0;
+      if (round == 0) {
+        if (ql < es.qvalid) {
+          float m = ninf;
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-              acc[i][j][4 * g + 0] *= sc.x;
-              acc[i][j][4 * g + 1] *= sc.y;
-              acc[i][j][4 * g + 2] *= sc.z;
-              acc[i][j][4 * g + 3] *= sc.w;
+          for (int rb = 0; rb < kRB; ++rb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) m = fmaxf(m, acc[rb][qb][j]);
+          if (m >= th) {
+#pragma unroll
+            for (int rb = 0; rb < kRB; ++rb)
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+                mask |= (acc[rb][qb][j] >= th ? 1u : 0u) << (rb * 4 + j);
+          }
+        }
+      } else {
+        mask = pending[qb];
+      }
+      pending[qb] = 0;
+      if (mask) {
+        any = true;
+        // stash this lane's scores of the block; walk only the passing ones
+        float *st = L.stash + tid * (4 * kRB);
+#pragma unroll
+        for (int rb = 0; rb < kRB; ++rb)
+          *reinterpret_cast<float4 *>(st + 4 * rb) =
+              make_float4(acc[rb][qb][0], acc[rb][qb][1], acc[rb][qb][2], acc[rb][qb][3]);
+        uint32_t mm = mask;
+        while (mm) {
+          const int idx = __builtin_ctz(mm);
+          const int slot = atomicAdd(&L.qcount[ql], 1);
+          if (slot >= kQcap) {
+            pending[qb] = mm;
+            break;
+          }
+          L.queue[ql * kQcap + slot] =
+              make_key(st[idx], (uint32_t)(rbase + (idx >> 2) * 16 + (idx & 3)));
+          mm &= mm - 1u;
+        }
+      }
+    }
+    if (__ballot(any)) {
+      if (lane == 0) L.flags[0] = es.epoch;
+    }
+    __syncthreads();
+    if (L.flags[0] != es.epoch) {
+      ++es.epoch;
+      break;
+    }
+    // merge queues into the k-lists, one thread per query
+    if (tid < es.qvalid) {
+      const int c = L.qcount[tid];
+      if (c > 0) {
+        const int n = c < kQcap ? c : kQcap;
+        uint64_t *l = LDS_LISTS ? L.ts.lists + tid * a.k
+                                : a.part + ((int64_t)(es.qbase + tid) * es.S + es.s_) * a.k;
+        uint64_t mn = L.ts.lmin[tid];
+        int mp = L.ts.lpos[tid];
+        for (int e = 0; e < n; ++e) {
+          const uint64_t key = L.queue[tid * kQcap + e];
+          if (key > mn) {
+            l[mp] = key;
+            mn = ~0ull;
+            for (int j2 = 0; j2 < a.k; ++j2) {
+              const uint64_t x = l[j2];
+              if (x < mn) {
+                mn = x;
+                mp = j2;
+              }
             }
           }
+        }
+        L.ts.lmin[tid] = mn;
+        L.ts.lpos[tid] = mp;
+        const float t = mn ? unord_score((uint32_t)(mn >> 32)) : ninf;
+        const float t0v = L.thr0[tid];
+        L.ts.thr[tid] = t > t0v ? t : t0v;
+        L.qcount[tid] = 0;
+        if (c > kQcap) L.flags[1] = es.epoch;
       }
-      bool hit0 = false, hit1 = false;
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          hit0 |= acc[i][0][e] >= tq0;
-          hit1 |= acc[i][1][e] >= tq1;
-        }
-      const int qc0 = wq * 64 + (lane & 31), qc1 = qc0 + 32;
-      if (hit0) ts.flag[qc0] = 1;
-      if (hit1) ts.flag[qc1] = 1;
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int r = wr * 64 + i * 32 + 8 * g + rsub;
-          float4 v0 = make_float4(acc[i][0][4 * g], acc[i][0][4 * g + 1], acc[i][0][4 * g + 2],
-                                  acc[i][0][4 * g + 3]);
-          float4 v1 = make_float4(acc[i][1][4 * g], acc[i][1][4 * g + 1], acc[i][1][4 * g + 2],
-                                  acc[i][1][4 * g + 3]);
-          *reinterpret_cast<float4 *>(dump + qc0 * kDumpLd + r) = v0;
-          *reinterpret_cast<float4 *>(dump + qc1 * kDumpLd + r) = v1;
-        }
-      __syncthreads();
-      scan_tile<kMQ, kNC, kDumpLd>(ts, a, dump, qbase, nu, rbase, sp.S, s);
-      __syncthreads();
-      tq0 = ts.thr[qc0];
-      tq1 = ts.thr[qc1];
     }
-    flush_lists<kMQ>(ts, a, qbase, nu, sp.S, s);
+    __syncthreads();
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb) thr_r[qb] = L.ts.thr[qb * 16 + cq];
+    const bool again = L.flags[1] == es.epoch;
+    ++es.epoch;
+    if (!again) break;
+  }
+}
+
+template <bool LDS_LISTS>
+__device__ __forceinline__ Lds2 carve_lds(unsigned char *p) {
+  Lds2 L;
+  L.bring = reinterpret_cast<uint16_t *>(p); p += 3 * kMQ2 * kKC2 * 2;
+  L.queue = reinterpret_cast<uint64_t *>(p); p += kMQ2 * kQcap * 8;
+  L.qcount = reinterpret_cast<int32_t *>(p); p += kMQ2 * 4;
+  L.thr0 = reinterpret_cast<float *>(p); p += kMQ2 * 4;
+  L.sscale = reinterpret_cast<float *>(p); p += kNC2 * 4;
+  L.flags = reinterpret_cast<int32_t *>(p); p += 16;
+  L.stash = reinterpret_cast<float *>(p); p += kT2 * kRB * 4 * 4;
+  L.gm = reinterpret_cast<float *>(p); p += kMQ2 * kLanesQ * kRB * 4;
+  L.ts.lmin = reinterpret_cast<uint64_t *>(p); p += kMQ2 * 8;
+  L.ts.lpos = reinterpret_cast<int32_t *>(p); p += kMQ2 * 4;
+  L.ts.thr = reinterpret_cast<float *>(p); p += kMQ2 * 4;
+  L.ts.flag = reinterpret_cast<int32_t *>(p); p += kMQ2 * 4;
+  L.ts.lists = LDS_LISTS ? reinterpret_cast<uint64_t *>(p) : nullptr;
+  return L;
+}
+
+template <bool FP8>
+__device__ __forceinline__ void mfma_chunk(f32x4 (&acc)[kRB][kQB], const uint4 (&ab)[kRB][2],
+                                           const uint16_t *bs, int cq, int lg) {
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    bf16x8 af[kRB];
+#pragma unroll
+    for (int rb = 0; rb < kRB; ++rb) {
+      if constexpr (FP8) {
+        const uint4 v = ab[rb][0];
+        af[rb] = s == 0 ? fp8x8_to_bf16(v.x, v.y) : fp8x8_to_bf16(v.z, v.w);
+      } else {
+        af[rb] = __builtin_bit_cast(bf16x8, ab[rb][s]);
+      }
+    }
+    // rows qb*16 + cq share (q & 7) with cq, so the swizzle of every query
+    // block is the one of block 0 shifted by qb*16 rows
+    const uint16_t *bsq = bs + swz(cq, kpiece<FP8>(lg, s));
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb) {
+      const bf16x8 bf = *reinterpret_cast<const bf16x8 *>(bsq + qb * 16 * kKC2);
+#pragma unroll
+      for (int rb = 0; rb < kRB; ++rb)
+        acc[rb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[rb], bf, acc[rb][qb], 0, 0, 0);
+    }
+  }
+}
+
+// FAST: d is a multiple of 64 * kRing and N >= kNC2.  Then no load ever needs
+// a per-lane clamp: every K chunk is whole, the ring turns a whole number of
+// times per tile, and the last (ragged) corpus tile is loaded shifted back to
+// end at row N, with the rows already scored by the previous tile excluded in
+// the epilogue.  Stream positions advance with scalar counters.  Otherwise
+// (general d or tiny N) loads clamp per lane and the K walk is padded.
+template <bool FP8, bool LDS_LISTS, bool FAST>
+__global__ __launch_bounds__(kT2, 1) void score_partial_mfma(ScoreArgs a) {
+  static_assert(kT2 == 256, "one wave per SIMD");
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const Lds2 L = carve_lds<LDS_LISTS>(smem);
+
+  const int64_t nu = read_nu(a.n_unique, a.n_unique_dev, a.cap);
+  const Split sp = split_for(nu, a.N, kMQ2, kNC2, a.grid, a.k);
+  const int items = (int)(sp.qtiles * sp.S);
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int cq = lane & 15, lg = lane >> 4;
+  const int N = (int)a.N, d = (int)a.d;
+  const int nch = (d + kKC2 - 1) / kKC2;
+  const float ninf = -__builtin_inff();
+  constexpr int kBP = (kMQ2 * 8 + kT2 - 1) / kT2;   // query pieces per thread
+  constexpr int esz = FP8 ? 1 : 2;
+  if (tid < 4) L.flags[tid] = 0;
+  EpiState es;
+  es.epoch = 1;
+
+  // per-lane corpus rows inside a tile and columns inside a chunk
+  int arow[kRB];
+#pragma unroll
+  for (int rb = 0; rb < kRB; ++rb) arow[rb] = wv * (16 * kRB) + rb * 16 + cq;
+  int acol[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) acol[s] = FP8 ? 16 * lg : 8 * (lg + 4 * s);
+  // FAST: byte offsets of this lane's corpus pieces from a tile/chunk base
+  uint32_t aoff[kRB][2];
+#pragma unroll
+  for (int rb = 0; rb < kRB; ++rb)
+#pragma unroll
+    for (int s = 0; s < 2; ++s) aoff[rb][s] = (uint32_t)(arow[rb] * d + acol[s]) * esz;
+
+  for (int w = logical_wg(a.grid); w < items; w += a.grid) {
+    const int qt = w % (int)sp.qtiles;
+    es.s_ = w / (int)sp.qtiles;
+    es.S = sp.S;
+    const int t0 = (int)((int64_t)es.s_ * sp.ntiles / sp.S);
+    const int t1 = (int)((int64_t)(es.s_ + 1) * sp.ntiles / sp.S);
+    es.qbase = qt * kMQ2;
+    es.qvalid = (int)(nu - es.qbase < kMQ2 ? nu - es.qbase : kMQ2);
+    const uint16_t *qtile = (const uint16_t *)a.q + (int64_t)es.qbase * d;
+    init_lists<kMQ2>(L.ts, a, es.qbase, nu, sp.S, es.s_);
+    for (int q = tid; q < kMQ2; q += kT2) {
+      L.qcount[q] = 0;
+      L.thr0[q] = ninf;
+    }
+    float thr_r[kQB];
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb) thr_r[qb] = ninf;
+
+    // query pieces this thread stages (global offset always readable; pieces
+    // of padding queries repeat the last real query and are never used)
+    int brow[kBP], bpc[kBP], bdst[kBP];
+    uint32_t bok = 0;
+#pragma unroll
+    for (int i = 0; i < kBP; ++i) {
+      const int piece = tid + kT2 * i;
+      const int q = piece >> 3, pp = piece & 7;
+      if (piece < kMQ2 * 8 && q < es.qvalid) bok |= 1u << i;
+      brow[i] = (q < es.qvalid ? q : es.qvalid - 1) * d;
+      bpc[i] = 8 * pp;
+      bdst[i] = piece < kMQ2 * 8 ? swz(q, pp) : swz(0, 0);
+    }
+
+    const int nchp = FAST ? nch : (nch + kRing - 1) / kRing * kRing;
+    const int ntl = t1 - t0;
+    const int total = ntl * nchp;
+    uint4 abuf[kRing][kRB][2];
+    uint4 bst[kBP];
+    // first corpus row loaded for a tile (FAST shifts the ragged last tile)
+    auto tile_row0 = [&](int tile) {
+      int r0 = tile * kNC2;
+      if (FAST && r0 > N - kNC2) r0 = N - kNC2;
+      return r0;
+    };
+    // stream positions (FAST): next corpus chunk to load, next query chunk
+    int a_tl = 0, a_kc = 0, b_kc = 0, b_slot = 0, r_slot = 0;
+    auto load_a = [&](int g, uint4 (&dst)[kRB][2]) {
+      if constexpr (FAST) {
+        const int tl = a_tl < ntl ? a_tl : ntl - 1;
+        const unsigned char *base = (const unsigned char *)a.corpus +
+                                    ((int64_t)tile_row0(t0 + tl) * d + a_kc * kKC2) * esz;
+#pragma unroll
+        for (int rb = 0; rb < kRB; ++rb)
+#pragma unroll
+          for (int s = 0; s < (FP8 ? 1 : 2); ++s)
+            dst[rb][s] = *reinterpret_cast<const uint4 *>(base + aoff[rb][s]);
+        if (++a_kc == nch) {
+          a_kc = 0;
+          ++a_tl;
+        }
+      } else {
+        if (g > total - 1) g = total - 1;
+        const int tile = t0 + g / nchp;
+        int kc = (g % nchp) * kKC2;
+        if (kc > (nch - 1) * kKC2) kc = (nch - 1) * kKC2;   // padding chunk: any data
+        const int rmax = N - 1 - tile * kNC2;          // last valid row in tile
+        const int cmax = d - (FP8 ? 16 : 8) - kc;      // last valid piece column
+        const unsigned char *base = (const unsigned char *)a.corpus +
+                                    ((int64_t)tile * kNC2 * d + kc) * esz;
+#pragma unroll
+        for (int rb = 0; rb < kRB; ++rb) {
+          const int r = arow[rb] < rmax ? arow[rb] : rmax;
+#pragma unroll
+          for (int s = 0; s < (FP8 ? 1 : 2); ++s) {
+            const int c = acol[s] < cmax ? acol[s] : cmax;
+            dst[rb][s] = *reinterpret_cast<const uint4 *>(base + (uint32_t)(r * d + c) * esz);
+          }
+        }
+      }
+    };
+    auto load_b = [&](int g) {
+      int kc;
+      if constexpr (FAST) {
+        kc = b_kc * kKC2;
+      } else {
+        kc = (g % nchp) * kKC2;
+        if (kc > (nch - 1) * kKC2) kc = (nch - 1) * kKC2;
+      }
+      const uint16_t *base = qtile + kc;
+#pragma unroll
+      for (int i = 0; i < kBP; ++i) {
+        int col = bpc[i];
+        if (!FAST && kc + col > d - 8) col = d - 8 - kc;
+        bst[i] = *reinterpret_cast<const uint4 *>(base + brow[i] + col);
+      }
+    };
+    auto store_b = [&](int g) {
+      int slot, kc;
+      if constexpr (FAST) {
+        slot = b_slot;
+        if (++b_slot == 3) b_slot = 0;
+        if (++b_kc == nch) b_kc = 0;
+        kc = 0;
+      } else {
+        slot = g % 3;
+        kc = (g % nchp) * kKC2;
+      }
+      uint16_t *base = L.bring + slot * (kMQ2 * kKC2);
+#pragma unroll
+      for (int i = 0; i < kBP; ++i) {
+        uint4 v = bst[i];
+        if (!FAST) {
+          const bool ok = ((bok >> i) & 1u) && kc + bpc[i] < d;
+          v.x = ok ? v.x : 0u;
+          v.y = ok ? v.y : 0u;
+          v.z = ok ? v.z : 0u;
+          v.w = ok ? v.w : 0u;
+        }
+        if (tid + kT2 * i < kMQ2 * 8) *reinterpret_cast<uint4 *>(base + bdst[i]) = v;
+      }
+    };
+    if (total > 0) {
+      load_b(0);
+      store_b(0);
+      load_b(1);
+      store_b(1);
+#pragma unroll
+      for (int r = 0; r < kRing - 1; ++r) load_a(r, abuf[r]);
+    }
+    __syncthreads();
+
+    f32x4 acc[kRB][kQB];
+    for (int tl = 0; tl < ntl; ++tl) {
+      const int tile = t0 + tl;
+      const int row0 = tile_row0(tile);
+#pragma unroll
+      for (int rb = 0; rb < kRB; ++rb)
+#pragma unroll
+        for (int qb = 0; qb < kQB; ++qb) acc[rb][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (FP8) {
+        for (int t = tid; t < kNC2; t += kT2) {
+          const int r = row0 + t;
+          L.sscale[t] = r < N ? a.scale[r] : 0.0f;
+        }
+      }
+      for (int kc4 = 0; kc4 < nchp; kc4 += kRing) {
+#pragma unroll
+        for (int r = 0; r < kRing; ++r) {
+          const int g = tl * nchp + kc4 + r;
+          // issue order matters for the in-order vmcnt waits: the query
+          // chunk (stored to LDS at the end of this step) before the corpus
+          // chunk needed kRing-1 steps later
+          load_b(g + 2);
+          __builtin_amdgcn_sched_barrier(0);
+          load_a(g + kRing - 1, abuf[(r + kRing - 1) % kRing]);
+          __builtin_amdgcn_sched_barrier(0);
+          int slot;
+          if constexpr (FAST) {
+            slot = r_slot;
+            if (++r_slot == 3) r_slot = 0;
+          } else {
+            slot = g % 3;
+          }
+          mfma_chunk<FP8>(acc, abuf[r], L.bring + slot * (kMQ2 * kKC2), cq, lg);
+          store_b(g + 2);
+          __syncthreads();
+        }
+      }
+      tile_epilogue<FP8, LDS_LISTS>(L, a, acc, thr_r, es, row0, tile * kNC2, tl == 0);
+    }
+    flush_lists<kMQ2>(L.ts, a, es.qbase, nu, sp.S, es.s_);
     __syncthreads();
   }
 }
@@ -565,15 +866,16 @@ static size_t partial_bytes(int64_t cap, int64_t N, int mq, int nc, int k) {
 
 size_t score_workspace_bytes(int64_t cap, int64_t N, int k, int corpus_dtype) {
   if (corpus_dtype == HS_F32) return partial_bytes(cap, N, kVMQ, kVNC, k);
-  return partial_bytes(cap, N, kMQ, kNC, k);
+  return partial_bytes(cap, N, kMQ2, kNC2, k);
 }
 
 template <typename K>
-static hipError_t launch_with_lds(K kern, int grid, int lds, const ScoreArgs &a, hipStream_t st) {
+static hipError_t launch_with_lds(K kern, int grid, int threads, int lds, const ScoreArgs &a,
+                                  hipStream_t st) {
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), lds, st, a);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(threads), lds, st, a);
   return hipGetLastError();
 }
 
@@ -595,16 +897,23 @@ hipError_t launch_score_partial(const void *q, const void *corpus, const float *
   if (corpus_dtype == HS_F32) {
     a.grid = persistent_grid(false);
     int lds = valu_lds_bytes(lds_lists, k);
-    return lds_lists ? launch_with_lds(score_partial_valu<true>, a.grid, lds, a, st)
-                     : launch_with_lds(score_partial_valu<false>, a.grid, lds, a, st);
+    return lds_lists ? launch_with_lds(score_partial_valu<true>, a.grid, kThreads, lds, a, st)
+                     : launch_with_lds(score_partial_valu<false>, a.grid, kThreads, lds, a, st);
   }
   a.grid = persistent_grid(true);
-  int lds = mfma_lds_bytes(lds_lists, k);
-  if (corpus_dtype == HS_FP8_E4M3)
-    return lds_lists ? launch_with_lds(score_partial_mfma<true, true>, a.grid, lds, a, st)
-                     : launch_with_lds(score_partial_mfma<true, false>, a.grid, lds, a, st);
-  return lds_lists ? launch_with_lds(score_partial_mfma<false, true>, a.grid, lds, a, st)
-                   : launch_with_lds(score_partial_mfma<false, false>, a.grid, lds, a, st);
+  int lds = mfma2_lds_bytes(lds_lists, k);
+  const bool fast = d % (kKC2 * kRing) == 0 && N >= kNC2;
+#define HS_LAUNCH(F8, LL, FA) \
+  return launch_with_lds(score_partial_mfma<F8, LL, FA>, a.grid, kT2, lds, a, st)
+  if (corpus_dtype == HS_FP8_E4M3) {
+    if (lds_lists) { if (fast) HS_LAUNCH(true, true, true); HS_LAUNCH(true, true, false); }
+    if (fast) HS_LAUNCH(true, false, true);
+    HS_LAUNCH(true, false, false);
+  }
+  if (lds_lists) { if (fast) HS_LAUNCH(false, true, true); HS_LAUNCH(false, true, false); }
+  if (fast) HS_LAUNCH(false, false, true);
+  HS_LAUNCH(false, false, false);
+#undef HS_LAUNCH
 }
 
 hipError_t launch_topk_merge(const void *part, int64_t n_unique, const int64_t *nu_dev,
@@ -616,8 +925,8 @@ hipError_t launch_topk_merge(const void *part, int64_t n_unique, const int64_t *
   if (blocks <= 0) return hipSuccess;
   if (blocks > 65535) blocks = 65535;
   hipLaunchKernelGGL(topk_merge_kernel, dim3((unsigned)blocks), dim3(kMergeThreads), 0, st,
-                     (const uint64_t *)part, n_unique, nu_dev, cap, N, k, valu ? kVMQ : kMQ,
-                     valu ? kVNC : kNC, grid, out_s, out_i);
+                     (const uint64_t *)part, n_unique, nu_dev, cap, N, k, valu ? kVMQ : kMQ2,
+                     valu ? kVNC : kNC2, grid, out_s, out_i);
   return hipGetLastError();
 }
 
