@@ -162,69 +162,76 @@ __device__ void flush_lists(const TileState &ts, const ScoreArgs &a, int64_t qba
 
 // ---------------------------------------------------------------- MFMA path
 //
-// Workgroup = 4 waves (one per SIMD).  Tile = 256 corpus rows x MQ = 16*QB
-// queries; wave w owns rows [64w, 64w+64) of the tile for all MQ queries, as
-// 4 x QB MFMA 16x16x32 blocks (A = 16 corpus rows, B = 16 queries, fp32 C).
+// Workgroup = 4 waves (one per SIMD).  Tile = 256 corpus rows x 128 queries;
+// wave w owns rows [64w, 64w+64) of the tile for all 128 queries, as 2 x 4
+// MFMA 32x32x16 blocks (A = 32 corpus rows, B = 32 queries, fp32 C).  With a
+// single wave per SIMD the 32x32x16 form is the one that keeps the matrix
+// core busy back to back.
 //
 // Operand paths, per K chunk of 64:
 //   corpus: global -> registers directly (each wave loads only its own rows,
-//           so nothing is shared and no LDS is needed), one chunk ahead;
-//   queries: global -> registers -> a 3-slot LDS ring (two chunks ahead),
-//           XOR-swizzled by row so that fragment reads are conflict-free.
+//           so nothing is shared and no LDS is needed), a ring of chunks;
+//   queries: global -> registers -> a 3-slot LDS ring, XOR-swizzled by row
+//           so that fragment reads are conflict-free.
 // Only the query operand is read from LDS: 64 corpus rows reuse each query
 // fragment, which keeps LDS traffic near half of its bandwidth at full MFMA
 // rate.  Inside an MFMA the K order is free as long as A and B agree, so each
 // lane takes the k-slice of a chunk that makes its corpus loads contiguous.
 //
-// Top-k epilogue, per tile and query: each lane holds 16 scores of each of
-// its QB queries (4 rows of each row block).  It compares their maximum with
-// the query's running threshold (registers); only on a hit are single scores
-// appended to a small per-query LDS queue, which one thread per query then
-// merges into the query's k-list (replace-the-minimum).  A full queue stops
-// the lane at that score; it resumes there after the merge has raised the
-// threshold, so no candidate is lost and none is seen twice.  Before the
-// first tile of a work item is filtered, the threshold is seeded with the
-// smallest of at least k group maxima of that tile (the 16 lanes holding a
-// query each split their rows into groups): those maxima are k distinct
-// scores, so their minimum never exceeds the true k-th best score.
+// Top-k epilogue, per tile and query: each lane holds 32 scores of each of
+// its 4 queries (16 rows of each 32-row block).  It compares their maximum
+// with the query's running threshold (registers); only on a hit are single
+// scores appended to a small per-query LDS queue, which one thread per query
+// then merges into the query's k-list (replace-the-minimum).  A full queue
+// leaves the remaining passing scores pending for another round after the
+// merge has raised the threshold, so no candidate is lost and none is seen
+// twice.  Before the first tile of a work item is filtered, the threshold is
+// seeded with the smallest of at least k group maxima of that tile (the 8
+// lanes holding a query each split their rows into groups): those maxima are
+// k distinct scores, so their minimum never exceeds the true k-th best score.
 
 constexpr int kW2 = 4;                      // waves per workgroup (one per SIMD)
 constexpr int kT2 = kW2 * 64;               // threads per workgroup
-constexpr int kRB = 4;                      // 16-row blocks per wave
-constexpr int kNC2 = kW2 * 16 * kRB;        // 256 rows per tile
+constexpr int kRB = 2;                      // 32-row blocks per wave
+constexpr int kNC2 = kW2 * 32 * kRB;        // 256 rows per tile
 constexpr int kKC2 = 64;                    // K per chunk
 constexpr int kQcap = 16;                   // queue slots per query
-constexpr int kLanesQ = kW2 * 4;            // lanes holding one query in a tile
-constexpr int kQB = 7;                      // query blocks of 16 per tile
-constexpr int kMQ2 = 16 * kQB;              // 112 queries per tile
+constexpr int kLanesQ = kW2 * 2;            // lanes holding one query in a tile
+constexpr int kQB = 4;                      // query blocks of 32 per tile
+constexpr int kMQ2 = 32 * kQB;              // 128 queries per tile
+constexpr int kVals = 16 * kRB;             // scores per lane and query per tile
 constexpr int kRing = 2;                    // corpus chunks held in registers
+constexpr int kBP = kMQ2 * 8 / kT2;         // query pieces staged per thread
+static_assert(kMQ2 * 8 % kT2 == 0, "query pieces divide evenly");
 
 struct Lds2 {
   uint16_t *bring;   // [3][MQ][64] bf16, swizzled
   uint64_t *queue;   // [MQ][kQcap]
-  float *gm;         // [MQ][kLanesQ * kRB] warm-up group maxima
   int32_t *qcount;   // [MQ]
   float *thr0;       // [MQ]
   float *sscale;     // [kNC2]
   int32_t *flags;    // [0] hit epoch, [1] overflow epoch
-  float *stash;      // [threads][4 * kRB] scores of one query block (rare path)
+  float *stash;      // [threads][kVals] scores of one query block (rare path)
+  float *gm;         // [MQ][kLanesQ * 8] warm-up group maxima (aliases stash)
   TileState ts;
 };
 
-// Warm-up groups per lane and query: the rows a lane holds for one query
-// are cut into gpl groups so that kLanesQ * gpl >= k group maxima exist; the
-// smallest of them is a valid lower bound for the k-th best score.  0 = no
-// warm-up (k too large).
+// Warm-up groups per lane and query: the kVals rows a lane holds for one
+// query are cut into gpl groups so that kLanesQ * gpl >= k group maxima exist;
+// the smallest of them is a valid lower bound for the k-th best score.
+// 0 = no warm-up (k too large).
 __host__ __device__ constexpr int warm_groups(int k) {
   int g = 1;
-  while (g <= kRB && kLanesQ * g < k) g <<= 1;
-  return g <= kRB ? g : 0;
+  while (g <= 8 && kLanesQ * g < k) g <<= 1;
+  return g <= 8 ? g : 0;
 }
+
+constexpr int kStashBytes = kT2 * kVals * 4 > kMQ2 * kLanesQ * 8 * 4 ? kT2 * kVals * 4
+                                                                      : kMQ2 * kLanesQ * 8 * 4;
 
 __host__ __device__ constexpr int mfma2_lds_bytes(bool lds_lists, int k) {
   return 3 * kMQ2 * kKC2 * 2 + kMQ2 * kQcap * 8 + kMQ2 * 4 + kMQ2 * 4 + kNC2 * 4 + 16 +
-         kT2 * kRB * 4 * 4 + kMQ2 * kLanesQ * kRB * 4 + kMQ2 * (8 + 4 + 4 + 4) +
-         (lds_lists ? kMQ2 * k * 8 : 0);
+         kStashBytes + kMQ2 * (8 + 4 + 4 + 4) + (lds_lists ? kMQ2 * k * 8 : 0);
 }
 
 __device__ __forceinline__ void cvt_fp8x4_to_bf16(uint32_t w, uint32_t &lo, uint32_t &hi) {
@@ -243,12 +250,13 @@ __device__ __forceinline__ bf16x8 fp8x8_to_bf16(uint32_t lo, uint32_t hi) {
   return __builtin_bit_cast(bf16x8, v);
 }
 
-// piece (16 bytes = 8 bf16) of a 64-wide K chunk that lane group g feeds to
-// MFMA step s: bf16 corpus rows are loaded as two contiguous 64-byte halves,
-// fp8 rows as one 16-byte slice per lane group
+// 16-byte piece (8 bf16) of a 64-wide K chunk that lane half h feeds to MFMA
+// step s.  bf16 corpus rows: the two lane halves load adjacent pieces, so each
+// load instruction reads 32 contiguous bytes per row; fp8 rows: each lane
+// loads 32 contiguous bytes (4 steps' worth) at once.
 template <bool FP8>
-__device__ __forceinline__ int kpiece(int g, int s) {
-  return FP8 ? 2 * g + s : g + 4 * s;
+__device__ __forceinline__ int kpiece(int h, int s) {
+  return FP8 ? 4 * h + s : 2 * s + h;
 }
 
 __device__ __forceinline__ int swz(int q, int p) { return q * 64 + ((p ^ (q & 7)) << 3); }
@@ -260,31 +268,38 @@ struct EpiState {
   int epoch;
 };
 
+// Row of score j of 32-row block rb held by a lane: 8*(j/4) + 4*h + j%4.
+__device__ __forceinline__ int acc_row(int rbase, int rb, int j) {
+  return rbase + rb * 32 + 8 * (j >> 2) + (j & 3);
+}
+
 // Top-k epilogue of one corpus tile.  `row0` is the corpus row of the tile's
 // first loaded row; rows below `rlo` (already scored by the previous tile)
 // and at or above N are excluded.
 template <bool FP8, bool LDS_LISTS>
 __device__ __forceinline__ void tile_epilogue(const Lds2 &L, const ScoreArgs &a,
-                                              f32x4 (&acc)[kRB][kQB], float (&thr_r)[kQB],
+                                              f32x16 (&acc)[kRB][kQB], float (&thr_r)[kQB],
                                               EpiState &es, int row0, int rlo, bool first) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int cq = lane & 15, lg = lane >> 4;
+  const int c = lane & 31, h = lane >> 5;
   const int N = (int)a.N;
   const float ninf = -__builtin_inff();
-  const int rbase = row0 + wv * (16 * kRB) + 4 * lg;   // + 16*rb + j
+  const int rbase = row0 + wv * (32 * kRB) + 4 * h;
   if (FP8) {
 #pragma unroll
-    for (int rb = 0; rb < kRB; ++rb) {
-      const float4 sc =
-          *reinterpret_cast<const float4 *>(L.sscale + wv * (16 * kRB) + rb * 16 + 4 * lg);
+    for (int rb = 0; rb < kRB; ++rb)
 #pragma unroll
-      for (int qb = 0; qb < kQB; ++qb) {
-        acc[rb][qb][0] *= sc.x;
-        acc[rb][qb][1] *= sc.y;
-        acc[rb][qb][2] *= sc.z;
-        acc[rb][qb][3] *= sc.w;
+      for (int jj = 0; jj < 4; ++jj) {
+        const float4 sc = *reinterpret_cast<const float4 *>(
+            L.sscale + wv * (32 * kRB) + rb * 32 + 8 * jj + 4 * h);
+#pragma unroll
+        for (int qb = 0; qb < kQB; ++qb) {
+          acc[rb][qb][4 * jj + 0] *= sc.x;
+          acc[rb][qb][4 * jj + 1] *= sc.y;
+          acc[rb][qb][4 * jj + 2] *= sc.z;
+          acc[rb][qb][4 * jj + 3] *= sc.w;
+        }
       }
-    }
   }
   // excluded rows never compete: NaN fails every >= test and is ignored by
   // fmaxf
@@ -292,8 +307,8 @@ __device__ __forceinline__ void tile_epilogue(const Lds2 &L, const ScoreArgs &a,
 #pragma unroll
     for (int rb = 0; rb < kRB; ++rb)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = rbase + rb * 16 + j;
+      for (int j = 0; j < 16; ++j) {
+        const int r = acc_row(rbase, rb, j);
         if (r >= N || r < rlo)
 #pragma unroll
           for (int qb = 0; qb < kQB; ++qb) acc[rb][qb][j] = __builtin_nanf("");
@@ -302,24 +317,26 @@ __device__ __forceinline__ void tile_epilogue(const Lds2 &L, const ScoreArgs &a,
   const int gpl = warm_groups(a.k);
   if (first && gpl > 0) {
     // warm-up threshold: the smallest of kLanesQ * gpl group maxima
-    const int span = kRB / gpl;   // row blocks per group
+    const int span = kVals / gpl;   // scores per group
 #pragma unroll
     for (int qb = 0; qb < kQB; ++qb) {
-      float *dst = L.gm + (qb * 16 + cq) * (kLanesQ * kRB) + (wv * 4 + lg) * gpl;
+      float *dst = L.gm + (qb * 32 + c) * (kLanesQ * 8) + (wv * 2 + h) * gpl;
       float m = ninf;
 #pragma unroll
-      for (int rb = 0; rb < kRB; ++rb) {
+      for (int rb = 0; rb < kRB; ++rb)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) m = fmaxf(m, acc[rb][qb][j]);
-        if ((rb + 1) % span == 0) {
-          dst[rb / span] = m;
-          m = ninf;
+        for (int j = 0; j < 16; ++j) {
+          m = fmaxf(m, acc[rb][qb][j]);
+          const int idx = rb * 16 + j;
+          if ((idx + 1) % span == 0) {
+            dst[idx / span] = m;
+            m = ninf;
+          }
         }
-      }
     }
     __syncthreads();
     if (tid < es.qvalid) {
-      const float *v = L.gm + tid * (kLanesQ * kRB);
+      const float *v = L.gm + tid * (kLanesQ * 8);
       const int n = kLanesQ * gpl;
       float mn = v[0];
       for (int i = 1; i < n; ++i) mn = fminf(mn, v[i]);
@@ -328,7 +345,7 @@ __device__ __forceinline__ void tile_epilogue(const Lds2 &L, const ScoreArgs &a,
     }
     __syncthreads();
 #pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) thr_r[qb] = L.ts.thr[qb * 16 + cq];
+    for (int qb = 0; qb < kQB; ++qb) thr_r[qb] = L.ts.thr[qb * 32 + c];
   }
 
   // candidate rounds: scores at or above the query threshold go to the
@@ -336,11 +353,12 @@ __device__ __forceinline__ void tile_epilogue(const Lds2 &L, const ScoreArgs &a,
   uint32_t pending[kQB];
 #pragma unroll
   for (int qb = 0; qb < kQB; ++qb) pending[qb] = 0;
+  float *st = L.stash + tid * kVals;
   for (int round = 0;; ++round) {
     bool any = false;
 #pragma unroll
     for (int qb = 0; qb < kQB; ++qb) {
-      const int ql = qb * 16 + cq;
+      const int ql = qb * 32 + c;
       const float th = thr_r[qb];
       uint32_t mask = 0;
       if (round == 0) {
@@ -349,13 +367,13 @@ __device__ __forceinline__ void tile_epilogue(const Lds2 &L, const ScoreArgs &a,
 #pragma unroll
           for (int rb = 0; rb < kRB; ++rb)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) m = fmaxf(m, acc[rb][qb][j]);
+            for (int j = 0; j < 16; ++j) m = fmaxf(m, acc[rb][qb][j]);
           if (m >= th) {
 #pragma unroll
             for (int rb = 0; rb < kRB; ++rb)
 #pragma unroll
-              for (int j = 0; j < 4; ++j)
-                mask |= (acc[rb][qb][j] >= th ? 1u : 0u) << (rb * 4 + j);
+              for (int j = 0; j < 16; ++j)
+                mask |= (acc[rb][qb][j] >= th ? 1u : 0u) << (rb * 16 + j);
           }
         }
       } else {
@@ -365,11 +383,13 @@ __device__ __forceinline__ void tile_epilogue(const Lds2 &L, const ScoreArgs &a,
       if (mask) {
         any = true;
         // stash this lane's scores of the block; walk only the passing ones
-        float *st = L.stash + tid * (4 * kRB);
 #pragma unroll
         for (int rb = 0; rb < kRB; ++rb)
-          *reinterpret_cast<float4 *>(st + 4 * rb) =
-              make_float4(acc[rb][qb][0], acc[rb][qb][1], acc[rb][qb][2], acc[rb][qb][3]);
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+            *reinterpret_cast<float4 *>(st + rb * 16 + 4 * jj) =
+                make_float4(acc[rb][qb][4 * jj], acc[rb][qb][4 * jj + 1],
+                            acc[rb][qb][4 * jj + 2], acc[rb][qb][4 * jj + 3]);
         uint32_t mm = mask;
         while (mm) {
           const int idx = __builtin_ctz(mm);
@@ -379,7 +399,7 @@ __device__ __forceinline__ void tile_epilogue(const Lds2 &L, const ScoreArgs &a,
             break;
           }
           L.queue[ql * kQcap + slot] =
-              make_key(st[idx], (uint32_t)(rbase + (idx >> 2) * 16 + (idx & 3)));
+              make_key(st[idx], (uint32_t)acc_row(rbase, idx >> 4, idx & 15));
           mm &= mm - 1u;
         }
       }
@@ -394,9 +414,9 @@ __device__ __forceinline__ void tile_epilogue(const Lds2 &L, const ScoreArgs &a,
     }
     // merge queues into the k-lists, one thread per query
     if (tid < es.qvalid) {
-      const int c = L.qcount[tid];
-      if (c > 0) {
-        const int n = c < kQcap ? c : kQcap;
+      const int cnt = L.qcount[tid];
+      if (cnt > 0) {
+        const int n = cnt < kQcap ? cnt : kQcap;
         uint64_t *l = LDS_LISTS ? L.ts.lists + tid * a.k
                                 : a.part + ((int64_t)(es.qbase + tid) * es.S + es.s_) * a.k;
         uint64_t mn = L.ts.lmin[tid];
@@ -421,12 +441,12 @@ __device__ __forceinline__ void tile_epilogue(const Lds2 &L, const ScoreArgs &a,
         const float t0v = L.thr0[tid];
         L.ts.thr[tid] = t > t0v ? t : t0v;
         L.qcount[tid] = 0;
-        if (c > kQcap) L.flags[1] = es.epoch;
+        if (cnt > kQcap) L.flags[1] = es.epoch;
       }
     }
     __syncthreads();
 #pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) thr_r[qb] = L.ts.thr[qb * 16 + cq];
+    for (int qb = 0; qb < kQB; ++qb) thr_r[qb] = L.ts.thr[qb * 32 + c];
     const bool again = L.flags[1] == es.epoch;
     ++es.epoch;
     if (!again) break;
@@ -442,8 +462,8 @@ __device__ __forceinline__ Lds2 carve_lds(unsigned char *p) {
   L.thr0 = reinterpret_cast<float *>(p); p += kMQ2 * 4;
   L.sscale = reinterpret_cast<float *>(p); p += kNC2 * 4;
   L.flags = reinterpret_cast<int32_t *>(p); p += 16;
-  L.stash = reinterpret_cast<float *>(p); p += kT2 * kRB * 4 * 4;
-  L.gm = reinterpret_cast<float *>(p); p += kMQ2 * kLanesQ * kRB * 4;
+  L.stash = reinterpret_cast<float *>(p);
+  L.gm = reinterpret_cast<float *>(p); p += kStashBytes;
   L.ts.lmin = reinterpret_cast<uint64_t *>(p); p += kMQ2 * 8;
   L.ts.lpos = reinterpret_cast<int32_t *>(p); p += kMQ2 * 4;
   L.ts.thr = reinterpret_cast<float *>(p); p += kMQ2 * 4;
@@ -452,32 +472,45 @@ __device__ __forceinline__ Lds2 carve_lds(unsigned char *p) {
   return L;
 }
 
+// One K chunk of MFMAs (every query block, including padding ones: a skip
+// per block would let the compiler chain MFMAs on one accumulator).
 template <bool FP8>
-__device__ __forceinline__ void mfma_chunk(f32x4 (&acc)[kRB][kQB], const uint4 (&ab)[kRB][2],
-                                           const uint16_t *bs, int cq, int lg) {
+__device__ __forceinline__ void mfma_chunk(f32x16 (&acc)[kRB][kQB], const uint4 (&ab)[kRB][4],
+                                           const uint16_t *bs, int c, int h) {
+  // all query fragments of the chunk are read up front: with one wave per
+  // SIMD nothing else would cover the LDS latency in front of each MFMA
+  // group (rows qb*32 + c share (q & 7) with c, so every block's swizzle is
+  // block 0's shifted by qb*32 rows)
+  bf16x8 bf[4][kQB];
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
+  for (int s = 0; s < 4; ++s) {
+    const uint16_t *bsq = bs + swz(c, kpiece<FP8>(h, s));
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb)
+      bf[s][qb] = *reinterpret_cast<const bf16x8 *>(bsq + qb * 32 * kKC2);
+  }
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
     bf16x8 af[kRB];
 #pragma unroll
     for (int rb = 0; rb < kRB; ++rb) {
       if constexpr (FP8) {
-        const uint4 v = ab[rb][0];
-        af[rb] = s == 0 ? fp8x8_to_bf16(v.x, v.y) : fp8x8_to_bf16(v.z, v.w);
+        const uint4 v = ab[rb][s >> 1];
+        af[rb] = (s & 1) == 0 ? fp8x8_to_bf16(v.x, v.y) : fp8x8_to_bf16(v.z, v.w);
       } else {
         af[rb] = __builtin_bit_cast(bf16x8, ab[rb][s]);
       }
     }
-    // rows qb*16 + cq share (q & 7) with cq, so the swizzle of every query
-    // block is the one of block 0 shifted by qb*16 rows
-    const uint16_t *bsq = bs + swz(cq, kpiece<FP8>(lg, s));
 #pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) {
-      const bf16x8 bf = *reinterpret_cast<const bf16x8 *>(bsq + qb * 16 * kKC2);
+    for (int qb = 0; qb < kQB; ++qb)
 #pragma unroll
       for (int rb = 0; rb < kRB; ++rb)
-        acc[rb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[rb], bf, acc[rb][qb], 0, 0, 0);
-    }
+        acc[rb][qb] =
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[rb], bf[s][qb], acc[rb][qb], 0, 0, 0);
   }
+  // keep that order through instruction scheduling: LDS reads, then MFMAs
+  __builtin_amdgcn_sched_group_barrier(0x100, 4 * kQB, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, 4 * kQB * kRB, 0);
 }
 
 // FAST: d is a multiple of 64 * kRing and N >= kNC2.  Then no load ever needs
@@ -496,29 +529,29 @@ __global__ __launch_bounds__(kT2, 1) void score_partial_mfma(ScoreArgs a) {
   const Split sp = split_for(nu, a.N, kMQ2, kNC2, a.grid, a.k);
   const int items = (int)(sp.qtiles * sp.S);
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int cq = lane & 15, lg = lane >> 4;
+  const int c = lane & 31, h = lane >> 5;
   const int N = (int)a.N, d = (int)a.d;
   const int nch = (d + kKC2 - 1) / kKC2;
   const float ninf = -__builtin_inff();
-  constexpr int kBP = (kMQ2 * 8 + kT2 - 1) / kT2;   // query pieces per thread
   constexpr int esz = FP8 ? 1 : 2;
+  constexpr int kAL = FP8 ? 2 : 4;   // 16-byte corpus loads per row block and chunk
   if (tid < 4) L.flags[tid] = 0;
   EpiState es;
   es.epoch = 1;
 
-  // per-lane corpus rows inside a tile and columns inside a chunk
+  // per-lane corpus rows inside a tile and byte columns inside a chunk
   int arow[kRB];
 #pragma unroll
-  for (int rb = 0; rb < kRB; ++rb) arow[rb] = wv * (16 * kRB) + rb * 16 + cq;
-  int acol[2];
+  for (int rb = 0; rb < kRB; ++rb) arow[rb] = wv * (32 * kRB) + rb * 32 + c;
+  int acol[4];   // element column of load i of a row block
 #pragma unroll
-  for (int s = 0; s < 2; ++s) acol[s] = FP8 ? 16 * lg : 8 * (lg + 4 * s);
+  for (int i = 0; i < 4; ++i) acol[i] = FP8 ? 32 * h + 16 * i : 8 * kpiece<false>(h, i);
   // FAST: byte offsets of this lane's corpus pieces from a tile/chunk base
-  uint32_t aoff[kRB][2];
+  uint32_t aoff[kRB][4];
 #pragma unroll
   for (int rb = 0; rb < kRB; ++rb)
 #pragma unroll
-    for (int s = 0; s < 2; ++s) aoff[rb][s] = (uint32_t)(arow[rb] * d + acol[s]) * esz;
+    for (int i = 0; i < 4; ++i) aoff[rb][i] = (uint32_t)(arow[rb] * d + acol[i]) * esz;
 
   for (int w = logical_wg(a.grid); w < items; w += a.grid) {
     const int qt = w % (int)sp.qtiles;
@@ -546,17 +579,17 @@ __global__ __launch_bounds__(kT2, 1) void score_partial_mfma(ScoreArgs a) {
     for (int i = 0; i < kBP; ++i) {
       const int piece = tid + kT2 * i;
       const int q = piece >> 3, pp = piece & 7;
-      if (piece < kMQ2 * 8 && q < es.qvalid) bok |= 1u << i;
+      if (q < es.qvalid) bok |= 1u << i;
       brow[i] = (q < es.qvalid ? q : es.qvalid - 1) * d;
       bpc[i] = 8 * pp;
-      bdst[i] = piece < kMQ2 * 8 ? swz(q, pp) : swz(0, 0);
+      bdst[i] = swz(q, pp);
     }
 
     const int nchp = FAST ? nch : (nch + kRing - 1) / kRing * kRing;
     const int ntl = t1 - t0;
     const int total = ntl * nchp;
-    uint4 abuf[kRing][kRB][2];
-    uint4 bst[kBP];
+    uint4 abuf[kRing][kRB][4];
+    uint4 bst[2][kBP];   // query chunks in flight: loaded one step before stored
     // first corpus row loaded for a tile (FAST shifts the ragged last tile)
     auto tile_row0 = [&](int tile) {
       int r0 = tile * kNC2;
@@ -565,7 +598,8 @@ __global__ __launch_bounds__(kT2, 1) void score_partial_mfma(ScoreArgs a) {
     };
     // stream positions (FAST): next corpus chunk to load, next query chunk
     int a_tl = 0, a_kc = 0, b_kc = 0, b_slot = 0, r_slot = 0;
-    auto load_a = [&](int g, uint4 (&dst)[kRB][2]) {
+    static_assert(kRing % 2 == 0, "query staging parity follows the ring");
+    auto load_a = [&](int g, uint4 (&dst)[kRB][4]) {
       if constexpr (FAST) {
         const int tl = a_tl < ntl ? a_tl : ntl - 1;
         const unsigned char *base = (const unsigned char *)a.corpus +
@@ -573,8 +607,8 @@ __global__ __launch_bounds__(kT2, 1) void score_partial_mfma(ScoreArgs a) {
 #pragma unroll
         for (int rb = 0; rb < kRB; ++rb)
 #pragma unroll
-          for (int s = 0; s < (FP8 ? 1 : 2); ++s)
-            dst[rb][s] = *reinterpret_cast<const uint4 *>(base + aoff[rb][s]);
+          for (int i = 0; i < kAL; ++i)
+            dst[rb][i] = *reinterpret_cast<const uint4 *>(base + aoff[rb][i]);
         if (++a_kc == nch) {
           a_kc = 0;
           ++a_tl;
@@ -592,17 +626,18 @@ __global__ __launch_bounds__(kT2, 1) void score_partial_mfma(ScoreArgs a) {
         for (int rb = 0; rb < kRB; ++rb) {
           const int r = arow[rb] < rmax ? arow[rb] : rmax;
 #pragma unroll
-          for (int s = 0; s < (FP8 ? 1 : 2); ++s) {
-            const int c = acol[s] < cmax ? acol[s] : cmax;
-            dst[rb][s] = *reinterpret_cast<const uint4 *>(base + (uint32_t)(r * d + c) * esz);
+          for (int i = 0; i < kAL; ++i) {
+            const int cc = acol[i] < cmax ? acol[i] : cmax;
+            dst[rb][i] = *reinterpret_cast<const uint4 *>(base + (uint32_t)(r * d + cc) * esz);
           }
         }
       }
     };
-    auto load_b = [&](int g) {
+    auto load_b = [&](int g, uint4 (&bs)[kBP]) {
       int kc;
       if constexpr (FAST) {
         kc = b_kc * kKC2;
+        if (++b_kc == nch) b_kc = 0;
       } else {
         kc = (g % nchp) * kKC2;
         if (kc > (nch - 1) * kKC2) kc = (nch - 1) * kKC2;
@@ -612,15 +647,14 @@ __global__ __launch_bounds__(kT2, 1) void score_partial_mfma(ScoreArgs a) {
       for (int i = 0; i < kBP; ++i) {
         int col = bpc[i];
         if (!FAST && kc + col > d - 8) col = d - 8 - kc;
-        bst[i] = *reinterpret_cast<const uint4 *>(base + brow[i] + col);
+        bs[i] = *reinterpret_cast<const uint4 *>(base + brow[i] + col);
       }
     };
-    auto store_b = [&](int g) {
+    auto store_b = [&](int g, const uint4 (&bs)[kBP]) {
       int slot, kc;
       if constexpr (FAST) {
         slot = b_slot;
         if (++b_slot == 3) b_slot = 0;
-        if (++b_kc == nch) b_kc = 0;
         kc = 0;
       } else {
         slot = g % 3;
@@ -629,7 +663,7 @@ __global__ __launch_bounds__(kT2, 1) void score_partial_mfma(ScoreArgs a) {
       uint16_t *base = L.bring + slot * (kMQ2 * kKC2);
 #pragma unroll
       for (int i = 0; i < kBP; ++i) {
-        uint4 v = bst[i];
+        uint4 v = bs[i];
         if (!FAST) {
           const bool ok = ((bok >> i) & 1u) && kc + bpc[i] < d;
           v.x = ok ? v.x : 0u;
@@ -637,27 +671,30 @@ __global__ __launch_bounds__(kT2, 1) void score_partial_mfma(ScoreArgs a) {
           v.z = ok ? v.z : 0u;
           v.w = ok ? v.w : 0u;
         }
-        if (tid + kT2 * i < kMQ2 * 8) *reinterpret_cast<uint4 *>(base + bdst[i]) = v;
+        *reinterpret_cast<uint4 *>(base + bdst[i]) = v;
       }
     };
     if (total > 0) {
-      load_b(0);
-      store_b(0);
-      load_b(1);
-      store_b(1);
+      load_b(0, bst[0]);
+      store_b(0, bst[0]);
+      load_b(1, bst[1]);
+      store_b(1, bst[1]);
+      load_b(2, bst[0]);
 #pragma unroll
       for (int r = 0; r < kRing - 1; ++r) load_a(r, abuf[r]);
     }
     __syncthreads();
 
-    f32x4 acc[kRB][kQB];
+    f32x16 acc[kRB][kQB];
     for (int tl = 0; tl < ntl; ++tl) {
       const int tile = t0 + tl;
       const int row0 = tile_row0(tile);
 #pragma unroll
       for (int rb = 0; rb < kRB; ++rb)
 #pragma unroll
-        for (int qb = 0; qb < kQB; ++qb) acc[rb][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int qb = 0; qb < kQB; ++qb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[rb][qb][e] = 0.0f;
       if (FP8) {
         for (int t = tid; t < kNC2; t += kT2) {
           const int r = row0 + t;
@@ -668,10 +705,12 @@ __global__ __launch_bounds__(kT2, 1) void score_partial_mfma(ScoreArgs a) {
 #pragma unroll
         for (int r = 0; r < kRing; ++r) {
           const int g = tl * nchp + kc4 + r;
-          // issue order matters for the in-order vmcnt waits: the query
-          // chunk (stored to LDS at the end of this step) before the corpus
-          // chunk needed kRing-1 steps later
-          load_b(g + 2);
+          // query chunk g+2 was loaded a full step ago; its LDS slot was last
+          // read in step g-1 (behind the previous barrier).  Then issue, in
+          // this order for the in-order vmcnt waits, the query chunk g+3 and
+          // the corpus chunk g+kRing-1.
+          store_b(g + 2, bst[r & 1]);
+          load_b(g + 3, bst[(r + 1) & 1]);
           __builtin_amdgcn_sched_barrier(0);
           load_a(g + kRing - 1, abuf[(r + kRing - 1) % kRing]);
           __builtin_amdgcn_sched_barrier(0);
@@ -682,8 +721,7 @@ __global__ __launch_bounds__(kT2, 1) void score_partial_mfma(ScoreArgs a) {
           } else {
             slot = g % 3;
           }
-          mfma_chunk<FP8>(acc, abuf[r], L.bring + slot * (kMQ2 * kKC2), cq, lg);
-          store_b(g + 2);
+          mfma_chunk<FP8>(acc, abuf[r], L.bring + slot * (kMQ2 * kKC2), c, h);
           __syncthreads();
         }
       }
