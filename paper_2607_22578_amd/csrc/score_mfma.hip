@@ -1,0 +1,976 @@
+// Steps 3 and 4 for bf16 and fp8-e4m3 corpora: score every distinct query
+// against the corpus on the matrix cores and keep the k best rows per query
+// and corpus slice.
+//
+// HeraSys runs one retrieval per fused node (Sec. 3.3 (I)) and batches ready
+// nodes of the same type (Appendix A, batching constraint); a retrieval
+// node's result is its Top-K chunks (Eq. 2 parameters; Sec. 4.1 workloads).
+// Here the batch is the n_u distinct queries and the retrieval is an exact
+// inner product, s[u, c] = scale_c * sum_j Q[u, j] C[c, j], accumulated in
+// fp32.
+//
+// Work decomposition: a persistent grid, one workgroup of four waves per CU.
+// A work item is (query tile of 128, corpus slice); a slice is a run of
+// tiles of 384 corpus rows.  Wave w owns rows [96w, 96w + 96) of a tile
+// against all 128 queries: 3 x 4 blocks of v_mfma_f32_32x32x16_bf16 with the
+// 192 fp32 accumulators in AGPRs (the rest of the register file holds two
+// sets of operand fragments and the epilogue's working set without spills).
+// Items of one slice get consecutive logical ids on one XCD, so the query
+// tiles that read the same corpus rows share that XCD's L2.
+//
+// Operand staging: both operands stream through a ring of LDS stages (two
+// for bf16, three for fp8), one K range of 64 per stage, written by
+// buffer_load ... lds (asynchronous copies from global memory straight into
+// LDS, no registers).  A bf16 corpus row contributes one 128-byte line per
+// stage (fp8: 64 bytes).  Every copy goes through a buffer descriptor whose
+// range covers exactly the valid rows of the tile (or query tile): rows past
+// N or past n_u, and the part of a last stage past d, read as zeros, so there
+// are no bounds branches and no access outside the operands.  Rows are stored
+// as 16-byte pieces with an XOR swizzle so that fragment reads (ds_read_b128)
+// are bank-conflict free.  Inside one MFMA the K order is free as long as
+// both operands agree; each lane takes the K slice that makes its fp8 corpus
+// piece one 16-byte read.
+//
+// Synchronisation per stage: after three of its four MFMA steps the waves
+// wait for their own copies of the next stage (s_waitcnt vmcnt with the exact
+// number of younger copies), then one barrier, then the next copies and the
+// next stage's first fragments, overlapped with the last step.  The fences
+// of __syncthreads are not used because they would wait for every copy in
+// flight.
+//
+// Top-k (fused, scores never reach memory), per tile: fp8 row scales
+// multiply the scores, rows past N are masked, and each lane compares the
+// maxima of its half blocks (8 scores) with the query's threshold; only
+// scores at or above it are appended to a small per-query LDS queue, merged
+// into the query's sorted k-list when a queue fills.  Thresholds come from
+// three lower bounds of the query's final k-th best score: the slice's own
+// k-list; a seed, the k-th largest of the lane maxima of a first pass over
+// one tile of every slice (a sample spread over the corpus); and the largest
+// bound any slice of the query has published so far (a per-query array in
+// the workspace, read asynchronously with each tile's copies).  Keys order
+// by (score desc, row asc): ties go to the lower corpus row independently of
+// tile, slice or lane.
+#include <type_traits>
+
+#include "common.h"
+
+namespace hs {
+
+typedef __bf16 bf16x8m __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2m __attribute__((ext_vector_type(2)));
+typedef float f32x16m __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int kMW = 4;                   // waves per workgroup (one per SIMD)
+constexpr int kMT = kMW * 64;            // threads
+constexpr int kMRB = 3;                  // 32-row blocks per wave
+constexpr int kMQB = 4;                  // 32-query blocks per tile
+constexpr int kMNC = kMW * 32 * kMRB;    // 384 corpus rows per tile
+constexpr int kMMQ = 32 * kMQB;          // 128 queries per tile
+constexpr int kMKC = 64;                 // K per ring stage (four 16-deep MFMA steps)
+constexpr int kMQcap = 8;                // queue slots per query and round
+constexpr int kMVals = 16 * kMRB;        // scores per lane and query per tile
+constexpr int kMLanesQ = kMW * 2;        // lanes holding one query in a tile
+constexpr int kMSplitMaxSK = 8192;       // bound on S*k (merge list length)
+constexpr int kMRowsW = 32 * kMRB;       // rows per wave in a tile
+constexpr int kMSS = kMNC + 128 - kMRowsW;  // row-scale slot stride (floats): the
+                                         // last wave's two 64-row copies overhang
+constexpr int kMLdsMax = 160 * 1024;     // LDS per workgroup on gfx950
+constexpr int kMGridMax = 512;           // persistent grid never exceeds this
+constexpr int kMGts = kMMQ + 32;         // shared-threshold slot stride (entries): the
+                                         // last wave's 64-entry copy overhangs
+
+template <bool FP8>
+struct Geo {
+  static constexpr int esz = FP8 ? 1 : 2;
+  static constexpr int arow = kMKC * esz;         // bytes of one corpus row per stage
+  static constexpr int abytes = kMNC * arow;
+  static constexpr int brow = kMKC * 2;           // bytes of one query row per stage
+  static constexpr int bbytes = kMMQ * brow;
+  static constexpr int stage = abytes + bbytes;
+  static constexpr int ns = FP8 ? 3 : 2;          // ring stages
+  static constexpr int nsc = FP8 ? ns + 1 : 0;    // row-scale slots (tiles in flight)
+  static constexpr int ngt = ns + 1;              // shared-threshold slots (tiles in flight)
+  static constexpr int adma = abytes / 1024 / kMW;  // 1 KiB copies per wave and stage
+  static constexpr int bdma = bbytes / 1024 / kMW;
+  static constexpr int ldma = adma + bdma;        // copies per wave and stage (scales aside)
+  static constexpr int apieces = arow / 16;       // 16-byte pieces of a corpus row stage
+  static constexpr int bpieces = brow / 16;
+};
+
+// Slot of 16-byte piece p in a row of P pieces: the 8 rows that fill the 32
+// banks once get distinct slots for the same p.
+template <int P>
+__device__ __forceinline__ int swz_slot(int p, int row) {
+  return p ^ ((row / (8 / P)) & (P - 1));
+}
+
+constexpr int kMWarmBytes = kMW * kMMQ * 4;   // per-wave warm-up minima (alias the queue)
+static_assert(kMWarmBytes <= kMMQ * kMQcap * 8, "warm-up minima fit in the queue");
+
+__host__ __device__ constexpr int mfma_lds_bytes(bool fp8, bool lds_lists, int k) {
+  return (fp8 ? Geo<true>::ns * Geo<true>::stage + Geo<true>::nsc * kMSS * 4 +
+                    Geo<true>::ngt * kMGts * 4
+              : Geo<false>::ns * Geo<false>::stage + Geo<false>::ngt * kMGts * 4) +
+         kMMQ * kMQcap * 8 + kMMQ * (4 + 4 + 4 + 8 + 4) + 16 +
+         (lds_lists ? kMMQ * k * 8 : 0);
+}
+
+// Warm-up groups per lane and query: the kMVals scores a lane holds for one
+// query are cut into gpl groups so that kMLanesQ * gpl >= k group maxima
+// exist.  0 = no warm-up (k too large for one tile).
+__host__ __device__ constexpr int mwarm_groups(int k) {
+  int g = 1;
+  while (g <= kMVals && kMLanesQ * g < k) g <<= 1;
+  return g <= kMVals ? g : 0;
+}
+
+__device__ __forceinline__ void cvt8_fp8_bf16(uint32_t lo, uint32_t hi, bf16x8m &out) {
+  // exact e4m3 -> bf16 (every e4m3 value is representable in bf16)
+  bf16x2m a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(lo, 1.0f, false);
+  bf16x2m b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(lo, 1.0f, true);
+  bf16x2m c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(hi, 1.0f, false);
+  bf16x2m e = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(hi, 1.0f, true);
+  uint4 v = make_uint4(__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b),
+                       __builtin_bit_cast(uint32_t, c), __builtin_bit_cast(uint32_t, e));
+  out = __builtin_bit_cast(bf16x8m, v);
+}
+
+// Barrier for LDS data: this wave's LDS operations complete, then s_barrier.
+// No memory fence, so copies into the ring stay in flight across it.
+__device__ __forceinline__ void bar_lds() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Wait until at most n of this wave's vector-memory operations are pending
+// (they complete in issue order).  n is one of the few values a ring depth
+// can produce.
+__device__ __forceinline__ void wait_vm(int n) {
+  __builtin_amdgcn_sched_barrier(0);
+  switch (n) {
+#define HS_VM_CASE(x) \
+  case x: asm volatile("s_waitcnt vmcnt(" #x ")" ::: "memory"); break;
+    HS_VM_CASE(1) HS_VM_CASE(2) HS_VM_CASE(3) HS_VM_CASE(4) HS_VM_CASE(5) HS_VM_CASE(6)
+    HS_VM_CASE(7) HS_VM_CASE(8) HS_VM_CASE(9) HS_VM_CASE(10) HS_VM_CASE(11) HS_VM_CASE(12)
+    HS_VM_CASE(13) HS_VM_CASE(14) HS_VM_CASE(15) HS_VM_CASE(16) HS_VM_CASE(17) HS_VM_CASE(18)
+    HS_VM_CASE(19) HS_VM_CASE(20) HS_VM_CASE(21) HS_VM_CASE(22) HS_VM_CASE(23) HS_VM_CASE(24)
+    HS_VM_CASE(25) HS_VM_CASE(26) HS_VM_CASE(27) HS_VM_CASE(28) HS_VM_CASE(29) HS_VM_CASE(30)
+    HS_VM_CASE(31) HS_VM_CASE(32)
+#undef HS_VM_CASE
+    default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+  }
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Buffer descriptor (raw, stride 0) over [base, base + bytes): loads at
+// offsets past `bytes` return zeros and touch no memory.
+typedef int i32x4m __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4m make_rsrc(const void *base, uint32_t bytes) {
+  // (the operands are wave-uniform; readfirstlane puts them in SGPRs)
+  const uint64_t p = (uint64_t)base;
+  i32x4m r;
+  r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)p);
+  r.y = __builtin_amdgcn_readfirstlane((int)((uint32_t)(p >> 32) & 0xFFFFu));
+  r.z = __builtin_amdgcn_readfirstlane((int)bytes);
+  r.w = 0x00020000;
+  return r;
+}
+
+// Asynchronous copies global -> LDS (buffer_load ... lds): lane l writes its
+// 16 (or 4) bytes at lds + 16 l (or 4 l).  They are issued from inline asm
+// on purpose: the compiler cannot tell which LDS bytes such a copy writes,
+// so for the builtin form it drains every copy in flight before any later
+// LDS read, which would defeat the ring.  The kernel orders the copies
+// itself (wait_vm, then a barrier).  M0 holds the LDS base; the compiler
+// reserves M0 and sets it before each of its own uses, so overwriting it
+// here is harmless.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(i32x4m rsrc, const void *lds, uint32_t voff) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(l), "v"(voff), "s"(rsrc) : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(i32x4m rsrc, const void *lds, uint32_t voff) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               :: "s"(l), "v"(voff), "s"(rsrc) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+struct MfmaArgs {
+  const void *q;
+  const void *corpus;
+  const float *scale;
+  int64_t N, d;
+  int k;
+  int64_t n_unique;
+  const int64_t *n_unique_dev;
+  int64_t cap;
+  int grid;
+  uint64_t *part;
+  uint32_t *gthr;   // [cap] per-query shared thresholds (ordered score, 0 = none)
+  uint32_t *lmax;   // [n_u][S][8] lane maxima of the seed pass (ordered scores)
+};
+
+// Fragments of one half stage (two 16-deep steps).  The K order inside a
+// stage is permuted identically for both operands: step t in 0..3 and lane
+// half h take elements [32h + 8t, 32h + 8t + 8), so that one 16-byte fp8
+// corpus piece feeds two consecutive steps.
+template <bool FP8>
+struct Frag {
+  // bf16: A pieces [step][rb]; fp8: raw 16-byte pieces [rb] (both steps)
+  uint4 a[FP8 ? 1 : 2][kMRB];
+  uint4 b[2][kMQB];
+};
+
+// Read half u of the stage in ring slot `st`.
+template <bool FP8>
+__device__ __forceinline__ void read_frags(Frag<FP8> &f, const unsigned char *st, int wv, int c,
+                                           int h, int u) {
+  using G = Geo<FP8>;
+  const unsigned char *abase = st + (wv * 32 * kMRB + c) * G::arow;
+  const unsigned char *bbase = st + G::abytes + c * G::brow;
+  if constexpr (FP8) {
+    const int slot = swz_slot<G::apieces>(2 * h + u, c);
+#pragma unroll
+    for (int rb = 0; rb < kMRB; ++rb)
+      f.a[0][rb] = *reinterpret_cast<const uint4 *>(abase + rb * 32 * G::arow + slot * 16);
+  } else {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int slot = swz_slot<G::apieces>(4 * h + 2 * u + s, c);
+#pragma unroll
+      for (int rb = 0; rb < kMRB; ++rb)
+        f.a[s][rb] = *reinterpret_cast<const uint4 *>(abase + rb * 32 * G::arow + slot * 16);
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int slot = swz_slot<G::bpieces>(4 * h + 2 * u + s, c);
+#pragma unroll
+    for (int qb = 0; qb < kMQB; ++qb)
+      f.b[s][qb] = *reinterpret_cast<const uint4 *>(bbase + qb * 32 * G::brow + slot * 16);
+  }
+}
+
+// Redefine the second step's operands of a half stage in place (no code):
+// MFMAs that use them cannot then be moved above a preceding barrier.
+typedef unsigned u32x4m __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void pin_u4(uint4 &v) {
+  u32x4m t = __builtin_bit_cast(u32x4m, v);
+  asm volatile("" : "+v"(t));
+  v = __builtin_bit_cast(uint4, t);
+}
+template <bool FP8>
+__device__ __forceinline__ void pin_step1(Frag<FP8> &f) {
+#pragma unroll
+  for (int rb = 0; rb < kMRB; ++rb) pin_u4(f.a[FP8 ? 0 : 1][rb]);
+#pragma unroll
+  for (int qb = 0; qb < kMQB; ++qb) pin_u4(f.b[1][qb]);
+}
+
+// One 16-deep MFMA step over the wave's 4 x 4 blocks.
+template <bool FP8, bool ZERO>
+__device__ __forceinline__ void mfma_step(f32x16m (&acc)[kMRB][kMQB], const Frag<FP8> &f,
+                                          int s) {
+  bf16x8m av[kMRB];
+#pragma unroll
+  for (int rb = 0; rb < kMRB; ++rb) {
+    if constexpr (FP8) {
+      const uint4 v = f.a[0][rb];
+      if (s == 0) cvt8_fp8_bf16(v.x, v.y, av[rb]);
+      else cvt8_fp8_bf16(v.z, v.w, av[rb]);
+    } else {
+      av[rb] = __builtin_bit_cast(bf16x8m, f.a[s][rb]);
+    }
+  }
+  const f32x16m zero = {};
+#pragma unroll
+  for (int rb = 0; rb < kMRB; ++rb)
+#pragma unroll
+    for (int qb = 0; qb < kMQB; ++qb)
+      acc[rb][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+          av[rb], __builtin_bit_cast(bf16x8m, f.b[s][qb]), ZERO ? zero : acc[rb][qb], 0, 0, 0);
+}
+
+struct MLds {
+  unsigned char *ring;
+  float *sscale;     // [nsc][kMSS] row scales of the tiles in flight (fp8)
+  uint32_t *gtl;     // [ngt][kMGts] shared thresholds of the tiles in flight
+  uint64_t *queue;   // [MQ][kMQcap] keys queued this round
+  int32_t *qcount;   // [MQ] keys queued (may exceed kMQcap: overflow)
+  float *thr0;       // [MQ] warm-up threshold of the item
+  float *thr;        // [MQ] current threshold
+  uint32_t *pub;     // [MQ] last threshold published to the shared array
+  uint64_t *lmin;    // [MQ] last (smallest) key of the sorted list, 0 while not full
+  float *warm;       // [kMW][MQ] per-wave minima of group maxima (aliases queue)
+  int32_t *flags;    // [1] overflow epoch, [2] half-full epoch
+  uint64_t *lists;   // [MQ][k] or nullptr (lists in the global partial buffer)
+};
+
+template <bool FP8, bool LDS_LISTS>
+__device__ __forceinline__ MLds carve_mlds(unsigned char *p, int k) {
+  using G = Geo<FP8>;
+  MLds L;
+  L.ring = p; p += G::ns * G::stage;
+  L.sscale = reinterpret_cast<float *>(p); p += G::nsc * kMSS * 4;
+  L.gtl = reinterpret_cast<uint32_t *>(p); p += G::ngt * kMGts * 4;
+  L.queue = reinterpret_cast<uint64_t *>(p);
+  L.warm = reinterpret_cast<float *>(p);   // (used before the queue in an epilogue)
+  p += kMMQ * kMQcap * 8;
+  L.lmin = reinterpret_cast<uint64_t *>(p); p += kMMQ * 8;
+  L.qcount = reinterpret_cast<int32_t *>(p); p += kMMQ * 4;
+  L.thr0 = reinterpret_cast<float *>(p); p += kMMQ * 4;
+  L.thr = reinterpret_cast<float *>(p); p += kMMQ * 4;
+  L.pub = reinterpret_cast<uint32_t *>(p); p += kMMQ * 4;
+  L.flags = reinterpret_cast<int32_t *>(p); p += 16;
+  L.lists = LDS_LISTS ? reinterpret_cast<uint64_t *>(p) : nullptr;
+  (void)k;
+  return L;
+}
+
+// Row of accumulator element i of 32-row block rb, relative to the tile.
+__device__ __forceinline__ int macc_row(int wv, int rb, int h, int i) {
+  return wv * 32 * kMRB + rb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+}
+
+struct MItem {
+  int qbase, qvalid, s;
+  int64_t S;
+};
+
+// Publish query t's threshold (a lower bound of its k-th best score over its
+// slice, hence over the whole corpus) to the per-query shared array: every
+// slice of the query filters with the largest bound any slice has reached.
+__device__ __forceinline__ void publish_thr(const MLds &L, const MfmaArgs &a, const MItem &it,
+                                            int t, float th) {
+  if (!(th > -__builtin_inff())) return;
+  const uint32_t o = ord_score(th);
+  if (o > L.pub[t]) {
+    L.pub[t] = o;
+    atomicMax(a.gthr + it.qbase + t, o);
+  }
+}
+
+// Merge the queued keys of query t into its k-list (one thread per query).
+// The list is kept sorted in descending key order (empty slots are key 0 at
+// the end), so its minimum is always the last entry and an insertion only
+// shifts the entries it passes: near the threshold, where nearly every
+// entrant lands, that is one or two steps.
+template <bool LDS_LISTS>
+__device__ __forceinline__ void merge_queue(const MLds &L, const MfmaArgs &a, const MItem &it,
+                                            int t) {
+  const int cnt = L.qcount[t];
+  if (cnt <= 0) return;
+  const int n = cnt < kMQcap ? cnt : kMQcap;
+  const int k = a.k;
+  uint64_t *l = LDS_LISTS ? L.lists + t * k
+                          : a.part + ((int64_t)(it.qbase + t) * it.S + it.s) * k;
+  uint64_t mn = L.lmin[t];
+  for (int e = 0; e < n; ++e) {
+    const uint64_t key = L.queue[t * kMQcap + e];
+    if (key > mn) {
+      int i = k - 1;
+      while (i > 0) {
+        const uint64_t prev = l[i - 1];
+        if (prev > key) break;
+        l[i] = prev;
+        --i;
+      }
+      l[i] = key;
+      mn = l[k - 1];
+    }
+  }
+  L.lmin[t] = mn;
+  const float tl = mn ? unord_score((uint32_t)(mn >> 32)) : -__builtin_inff();
+  const float t0v = L.thr0[t];
+  L.thr[t] = tl > t0v ? tl : t0v;
+  publish_thr(L, a, it, t, L.thr[t]);
+  L.qcount[t] = 0;
+}
+
+// Keep the accumulators in AGPRs and make the compiler forget any VGPR copy
+// of them: the epilogue then reads each element where it is used instead of
+// holding all 256 in VGPRs across its loops.
+__device__ __forceinline__ void pin_acc(f32x16m (&acc)[kMRB][kMQB]) {
+#pragma unroll
+  for (int rb = 0; rb < kMRB; ++rb)
+#pragma unroll
+    for (int qb = 0; qb < kMQB; ++qb) asm volatile("" : "+a"(acc[rb][qb]));
+}
+
+// An opaque copy of a lane value: values derived from it are recomputed
+// where they are used instead of being hoisted (and spilled) by the compiler.
+__device__ __forceinline__ int opaque(int x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+// Score of accumulator element (rb, qb, i) of this lane: fp8 row scale applied,
+// NaN for rows past N (NaN fails every >= test and fmaxf ignores it).  `lim`
+// = number of valid rows of the tile counted from this lane's first row.
+template <bool FP8>
+__device__ __forceinline__ float mscore(const f32x16m (&acc)[kMRB][kMQB], const float *ssc_lane,
+                                        int lim, int rb, int qb, int i) {
+  const int r = rb * 32 + 8 * (i >> 2) + (i & 3);
+  float v = acc[rb][qb][i];
+  if constexpr (FP8) v *= ssc_lane[r];
+  return r < lim ? v : __builtin_nanf("");
+}
+
+// Warm-up: per query, the smallest of this lane's group maxima (groups of
+// SPAN consecutive scores), combined over the two lane halves and stored per
+// wave.
+template <bool FP8, int SPAN>
+__device__ __forceinline__ void warm_minima(const MLds &L, f32x16m (&acc)[kMRB][kMQB],
+                                            const float *ssc_lane, int lim0, int wv, int c,
+                                            int h) {
+#pragma unroll
+  for (int qb = 0; qb < kMQB; ++qb) {
+    const int lim = opaque(lim0);
+    float mn = __builtin_inff(), m = -__builtin_inff();
+#pragma unroll
+    for (int rb = 0; rb < kMRB; ++rb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        m = fmaxf(m, mscore<FP8>(acc, ssc_lane, lim, rb, qb, i));
+        if ((rb * 16 + i + 1) % SPAN == 0) {
+          mn = fminf(mn, m);
+          m = -__builtin_inff();
+        }
+      }
+    mn = fminf(mn, __shfl_xor(mn, 32));
+    if (h == 0) L.warm[wv * kMMQ + qb * 32 + c] = mn;
+  }
+}
+
+// Seed pass: each lane's best score of the tile for each of its queries, as
+// an ordered score, to lmax[(query * S + slice) * 8 + lane-of-query].  These
+// are scores of distinct corpus rows, so the k-th largest of all of a
+// query's lane maxima (over all slices) is a lower bound of its k-th best
+// score over the whole corpus.
+template <bool FP8>
+__device__ __forceinline__ void mtile_lane_maxima(const MfmaArgs &a, const MItem &it,
+                                                  f32x16m (&acc)[kMRB][kMQB], int row0,
+                                                  const float *ssc) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int c = lane & 31, h = lane >> 5;
+  const int lrow = wv * 32 * kMRB + 4 * h;
+  const int lim0 = (int)a.N - row0 - lrow;
+  const float *ssc_lane = FP8 ? ssc + lrow : nullptr;
+  bar_lds();   // the tile's row scales are in LDS for every wave
+  pin_acc(acc);
+#pragma unroll
+  for (int qb = 0; qb < kMQB; ++qb) {
+    const int lim = opaque(lim0);
+    float m = -__builtin_inff();
+#pragma unroll
+    for (int rb = 0; rb < kMRB; ++rb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) m = fmaxf(m, mscore<FP8>(acc, ssc_lane, lim, rb, qb, i));
+    const int ql = qb * 32 + c;
+    if (ql < it.qvalid)
+      a.lmax[((int64_t)(it.qbase + ql) * it.S + it.s) * kMLanesQ + wv * 2 + h] =
+          m > -__builtin_inff() ? ord_score(m) : 0u;
+  }
+}
+
+// Top-k epilogue of one tile.  row0 = corpus row of the tile's first row;
+// ssc = row scales of the tile (fp8).
+template <bool FP8, bool LDS_LISTS>
+__device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a, const MItem &it,
+                                               f32x16m (&acc)[kMRB][kMQB],
+                                               float (&thr_r)[kMQB], int &epoch, int row0,
+                                               const float *ssc, const uint32_t *gt,
+                                               bool first) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int c = lane & 31, h = lane >> 5;
+  const float ninf = -__builtin_inff();
+  const int lrow = wv * 32 * kMRB + 4 * h;   // this lane's first row in the tile
+  const int lim0 = (int)a.N - row0 - lrow;
+  const float *ssc_lane = FP8 ? ssc + lrow : nullptr;
+  pin_acc(acc);
+  const int gpl = mwarm_groups(a.k);
+  if (first && gpl > 0) {
+    // warm-up threshold: the smallest of kMLanesQ * gpl group maxima (the
+    // queue, which these minima alias, is empty at an item's first tile)
+    bar_lds();
+    switch (gpl) {
+      case 1: warm_minima<FP8, kMVals / 1>(L, acc, ssc_lane, lim0, wv, c, h); break;
+      case 2: warm_minima<FP8, kMVals / 2>(L, acc, ssc_lane, lim0, wv, c, h); break;
+      case 4: warm_minima<FP8, kMVals / 4>(L, acc, ssc_lane, lim0, wv, c, h); break;
+      case 8: warm_minima<FP8, kMVals / 8>(L, acc, ssc_lane, lim0, wv, c, h); break;
+      case 16: warm_minima<FP8, kMVals / 16>(L, acc, ssc_lane, lim0, wv, c, h); break;
+      case 32: warm_minima<FP8, kMVals / 32>(L, acc, ssc_lane, lim0, wv, c, h); break;
+      default: warm_minima<FP8, 1>(L, acc, ssc_lane, lim0, wv, c, h); break;
+    }
+    bar_lds();
+    if (tid < it.qvalid) {
+      float th = L.warm[tid];
+#pragma unroll
+      for (int w = 1; w < kMW; ++w) th = fminf(th, L.warm[w * kMMQ + tid]);
+      L.thr0[tid] = th;
+      L.thr[tid] = th;
+      publish_thr(L, a, it, tid, th);
+    }
+    bar_lds();
+#pragma unroll
+    for (int qb = 0; qb < kMQB; ++qb) thr_r[qb] = L.thr[qb * 32 + c];
+  }
+
+  // shared thresholds of this lane's queries (read when the tile's copies
+  // started; a stale value is just a lower bound)
+  float g_r[kMQB];
+#pragma unroll
+  for (int qb = 0; qb < kMQB; ++qb) {
+    const uint32_t gq = gt[qb * 32 + c];
+    g_r[qb] = gq ? unord_score(gq) : -__builtin_inff();
+    thr_r[qb] = fmaxf(thr_r[qb], g_r[qb]);
+  }
+  // scores still to examine, 8 per byte (half of a 32-row block): the
+  // half blocks of this lane whose best score reaches the query threshold
+  pin_acc(acc);
+  uint64_t pend[kMQB];
+  const bool tail = lim0 < 32 * kMRB;   // some of this lane's rows may be past N
+#pragma unroll
+  for (int qb = 0; qb < kMQB; ++qb) {
+    const int lim = opaque(lim0);
+    const float th = thr_r[qb];
+    uint64_t p = 0;
+#pragma unroll
+    for (int hb = 0; hb < 2 * kMRB; ++hb) {
+      float m = ninf;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int i = 8 * (hb & 1) + j;
+        m = fmaxf(m, (!FP8 && !tail) ? acc[hb >> 1][qb][i]
+                                     : mscore<FP8>(acc, ssc_lane, lim, hb >> 1, qb, i));
+      }
+      p |= m >= th ? 0xFFull << (8 * hb) : 0ull;
+    }
+    pend[qb] = qb * 32 + c < it.qvalid ? p : 0ull;
+  }
+  // Scores at or above the current threshold are appended to the per-query
+  // LDS queues (atomics, no barrier).  Merges into the k-lists are deferred:
+  // one barrier per tile checks whether some queue overflowed (its
+  // candidates stay pending) or is half full; only then do the threads of
+  // the queries merge, the thresholds rise, and pending candidates are
+  // examined again.
+  for (;;) {
+    bool ovf = false, full = false;
+    pin_acc(acc);
+#pragma unroll
+    for (int qb = 0; qb < kMQB; ++qb) {
+      if (!__builtin_amdgcn_ballot_w64(pend[qb] != 0)) continue;
+      const int ql = qb * 32 + c;
+      const float th = thr_r[qb];
+      const int lim = opaque(lim0);
+      const int rowb = opaque(row0 + lrow);
+      uint64_t keep = 0;
+#pragma unroll
+      for (int hb = 0; hb < 2 * kMRB; ++hb) {
+        const int rb = hb >> 1, half = hb & 1;
+        const uint32_t m8 = (uint32_t)(pend[qb] >> (8 * hb)) & 0xFFu;
+        if (!__builtin_amdgcn_ballot_w64(m8 != 0)) continue;
+        // exact candidates of this half block under the current threshold
+        float v[8];
+        uint32_t cand = 0;
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          v[jj] = (!FP8 && !tail) ? acc[rb][qb][8 * half + jj]
+                                  : mscore<FP8>(acc, ssc_lane, lim, rb, qb, 8 * half + jj);
+          cand |= ((m8 >> jj) & 1u) && v[jj] >= th ? 1u << jj : 0u;
+        }
+        if (!__builtin_amdgcn_ballot_w64(cand != 0)) continue;
+        uint32_t rest = 0;
+        while (cand) {
+          const int jx = __builtin_ctz(cand);
+          float sc = v[0];
+#pragma unroll
+          for (int jj = 1; jj < 8; ++jj) sc = jx == jj ? v[jj] : sc;
+          const int slot = atomicAdd(&L.qcount[ql], 1);
+          if (slot >= kMQcap) {
+            rest = cand;
+            ovf = true;
+            break;
+          }
+          full |= slot + 1 >= kMQcap / 2;
+          const int r = rb * 32 + 16 * half + 8 * (jx >> 2) + (jx & 3);
+          L.queue[ql * kMQcap + slot] = make_key(sc, (uint32_t)(rowb + r));
+          cand &= cand - 1u;
+        }
+        keep |= (uint64_t)rest << (8 * hb);
+      }
+      pend[qb] = keep;
+    }
+    if (__builtin_amdgcn_ballot_w64(ovf) && lane == 0) L.flags[1] = epoch;
+    if (__builtin_amdgcn_ballot_w64(full) && lane == 0) L.flags[2] = epoch;
+    bar_lds();
+    const bool again = L.flags[1] == epoch;
+    if (!again && L.flags[2] != epoch) {   // no queue needs a merge yet
+      ++epoch;
+      break;
+    }
+    if (tid < it.qvalid) merge_queue<LDS_LISTS>(L, a, it, tid);
+    bar_lds();
+#pragma unroll
+    for (int qb = 0; qb < kMQB; ++qb) thr_r[qb] = fmaxf(L.thr[qb * 32 + c], g_r[qb]);
+    ++epoch;
+    if (!again) break;
+  }
+}
+
+template <bool FP8, bool LDS_LISTS, bool SEED>
+__global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
+  using G = Geo<FP8>;
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
+  const MLds L = carve_mlds<FP8, LDS_LISTS>(smem, a.k);
+
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int c = lane & 31, h = lane >> 5;
+  const int64_t nu = read_nu(a.n_unique, a.n_unique_dev, a.cap);
+  int64_t smax = kMSplitMaxSK / a.k;
+  const Split sp = make_split(nu, a.N, kMMQ, kMNC, a.grid, smax < 1 ? 1 : smax);
+  const int items = (int)(sp.qtiles * sp.S);
+  const int N = (int)a.N, d = (int)a.d;
+  const int nch = (d + kMKC - 1) / kMKC;
+  const float ninf = -__builtin_inff();
+  if (tid < 4) L.flags[tid] = 0;
+  int epoch = 1;
+
+  // (the per-lane copy offsets are recomputed at each copy from the lane id,
+  // a few VALU operations, rather than held in registers across the loop)
+  for (int w = logical_wg(a.grid); w < items; w += a.grid) {
+    MItem it;
+    const int qt = w % (int)sp.qtiles;
+    it.s = w / (int)sp.qtiles;
+    it.S = sp.S;
+    const int s0 = (int)((int64_t)it.s * sp.ntiles / sp.S);
+    const int s1 = (int)((int64_t)(it.s + 1) * sp.ntiles / sp.S);
+    const int t0 = s0;
+    const int t1 = SEED && s1 > s0 ? s0 + 1 : s1;
+    it.qbase = qt * kMMQ;
+    it.qvalid = (int)(nu - it.qbase < kMMQ ? nu - it.qbase : kMMQ);
+    const int ntl = t1 - t0;
+    const int T = ntl * nch;
+
+    // per-item state
+    if (tid < kMMQ) {
+      L.qcount[tid] = 0;
+      L.thr0[tid] = ninf;
+      L.thr[tid] = ninf;
+      L.lmin[tid] = 0ull;
+      L.pub[tid] = 0u;
+      if (tid < it.qvalid && !SEED) {
+        uint64_t *l = LDS_LISTS ? L.lists + tid * a.k
+                                : a.part + ((int64_t)(it.qbase + tid) * it.S + it.s) * a.k;
+        for (int j = 0; j < a.k; ++j) l[j] = 0ull;
+      }
+    }
+    float thr_r[kMQB];   // (read from L.thr after the prologue barrier)
+
+    const i32x4m qrs =
+        make_rsrc((const unsigned char *)a.q + (int64_t)it.qbase * d * 2,
+                  (uint32_t)(it.qvalid * d * 2));
+
+    // copy stream: next chunk to issue
+    int i_tl = 0, i_kc = 0, i_slot = 0, i_sc = 0, i_gt = 0, i_left = T;
+    auto issue = [&]() __attribute__((always_inline)) {
+      if (i_left <= 0) return;
+      const int row0 = (t0 + i_tl) * kMNC;
+      const int rows = N - row0 < kMNC ? N - row0 : kMNC;
+      const i32x4m ars =
+          make_rsrc((const unsigned char *)a.corpus + (int64_t)row0 * d * G::esz,
+                    (uint32_t)(rows * d * G::esz));
+      unsigned char *st = L.ring + i_slot * G::stage;
+      const int ln = opaque(lane);
+      // corpus copy j: 1 KiB = (64 / PA) rows of G::arow bytes; lane -> (row,
+      // slot), and the slot receives the piece that the swizzle puts there
+      constexpr int PA = G::apieces, PB = G::bpieces;
+      const int arow0 = wv * G::adma * (64 / PA) + ln / PA;
+      const uint32_t abase = (uint32_t)(arow0 * d * G::esz +
+                                        swz_slot<PA>(ln % PA, ln / PA) * 16 + i_kc * G::esz);
+#pragma unroll
+      for (int j = 0; j < G::adma; ++j)
+        dma16(ars, st + (wv * G::adma + j) * 1024,
+              abase + (uint32_t)(j * (64 / PA) * d * G::esz));
+      // query copy j: 1 KiB = (64 / PB) rows; pieces past d read as zeros
+      const int bpiece = swz_slot<PB>(ln % PB, ln / PB);
+      const bool bok = i_kc + bpiece * 8 < d;
+      const uint32_t bbase =
+          (uint32_t)(((wv * G::bdma * (64 / PB) + ln / PB) * d + bpiece * 8 + i_kc) * 2);
+#pragma unroll
+      for (int j = 0; j < G::bdma; ++j) {
+        const uint32_t vo = bok ? bbase + (uint32_t)(j * (64 / PB) * d * 2) : 0x80000000u;
+        dma16(qrs, st + G::abytes + (wv * G::bdma + j) * 1024, vo);
+      }
+      if (i_kc == 0) {
+        // shared thresholds of the query tile, entries [32 wv, 32 wv + 64)
+        const i32x4m grs = make_rsrc(a.gthr + it.qbase, (uint32_t)(it.qvalid * 4));
+        dma4(grs, L.gtl + i_gt * kMGts + 32 * wv, (uint32_t)((32 * wv + ln) * 4));
+        i_gt = i_gt + 1 == G::ngt ? 0 : i_gt + 1;
+      }
+      if constexpr (FP8) {
+        if (i_kc == 0) {
+          // rows [kMRowsW * wv, + 128) of the tile: the wave's own rows and an
+          // overlap with the next wave's (same values, same place)
+          const i32x4m srs = make_rsrc(a.scale + row0, (uint32_t)(rows * 4));
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            dma4(srs, L.sscale + i_sc * kMSS + wv * kMRowsW + j * 64,
+                 (uint32_t)((wv * kMRowsW + j * 64 + ln) * 4));
+          i_sc = i_sc + 1 == G::nsc ? 0 : i_sc + 1;
+        }
+      }
+      i_kc += kMKC;
+      if (i_kc >= d) {
+        i_kc = 0;
+        ++i_tl;
+      }
+      i_slot = i_slot + 1 == G::ns ? 0 : i_slot + 1;
+      --i_left;
+    };
+
+#pragma unroll
+    for (int j = 0; j < G::ns; ++j) issue();
+    // chunk 0 landed (younger copies: chunks 1 .. ns-1, at most T-1 of them)
+    {
+      const int younger = T - 1 < G::ns - 1 ? T - 1 : G::ns - 1;
+      wait_vm(younger > 0 ? younger * G::ldma : 0);
+    }
+    bar_lds();
+
+#pragma unroll
+    for (int qb = 0; qb < kMQB; ++qb) thr_r[qb] = L.thr[qb * 32 + c];
+    f32x16m acc[kMRB][kMQB];
+    Frag<FP8> f0, f1;
+    read_frags<FP8>(f0, L.ring, wv, c, h, 0);
+    int r_slot = 0, e_sc = 0, e_gt = 0, g = 0;
+
+    // one stage: two halves of two MFMA steps each; the second half carries
+    // the wait for the next stage, the barrier, the next copies and the
+    // next stage's first fragments, so that reads overlap the last MFMAs
+    auto stage = [&](auto first_c, bool rd) __attribute__((always_inline)) {
+      constexpr bool FIRST = decltype(first_c)::value;
+      mfma_step<FP8, FIRST>(acc, f0, 0);
+      read_frags<FP8>(f1, L.ring + r_slot * G::stage, wv, c, h, 1);
+      mfma_step<FP8, false>(acc, f0, 1);
+      mfma_step<FP8, false>(acc, f1, 0);
+      r_slot = r_slot + 1 == G::ns ? 0 : r_slot + 1;
+      if (g + 1 < T) {
+        // stage g+1 landed: younger copies are those of stages g+2 .. g+ns-1
+        const int younger = T - 2 - g < G::ns - 2 ? T - 2 - g : G::ns - 2;
+        wait_vm(younger > 0 ? younger * G::ldma : 0);
+        bar_lds();
+        issue();   // stage g+ns into the slot stage g used
+      }
+      pin_step1<FP8>(f1);
+      if (rd) read_frags<FP8>(f0, L.ring + r_slot * G::stage, wv, c, h, 0);
+      mfma_step<FP8, false>(acc, f1, 1);
+      ++g;
+    };
+    // (the first stage of a tile starts the accumulators from zero; its call
+    // is peeled so that the previous tile's accumulators are dead here.  The
+    // last stage of a tile leaves the next fragments in LDS: the epilogue runs
+    // with only the accumulators live, and f0 is refilled after it.)
+    for (int tl = 0; tl < ntl; ++tl) {
+      stage(std::true_type{}, nch > 1);
+      for (int j = 1; j < nch; ++j) stage(std::false_type{}, j + 1 < nch);
+      if constexpr (SEED)
+        mtile_lane_maxima<FP8>(a, it, acc, (t0 + tl) * kMNC,
+                               FP8 ? L.sscale + e_sc * kMSS : nullptr);
+      else
+        mtile_epilogue<FP8, LDS_LISTS>(L, a, it, acc, thr_r, epoch, (t0 + tl) * kMNC,
+                                       FP8 ? L.sscale + e_sc * kMSS : nullptr,
+                                       L.gtl + e_gt * kMGts, tl == 0);
+      if constexpr (FP8) e_sc = e_sc + 1 == G::nsc ? 0 : e_sc + 1;
+      e_gt = e_gt + 1 == G::ngt ? 0 : e_gt + 1;
+      read_frags<FP8>(f0, L.ring + r_slot * G::stage, wv, c, h, 0);
+    }
+
+    // merge what is still queued, then flush the LDS lists of this item
+    if constexpr (!SEED) {
+      bar_lds();
+      if (tid < it.qvalid) merge_queue<LDS_LISTS>(L, a, it, tid);
+    }
+    if (LDS_LISTS && !SEED) {
+      bar_lds();
+      const int tot = it.qvalid * a.k;
+      for (int t = tid; t < tot; t += kMT) {
+        const int q = t / a.k, j = t - q * a.k;
+        a.part[((int64_t)(it.qbase + q) * it.S + it.s) * a.k + j] = L.lists[t];
+      }
+    }
+    wait_vm(0);
+    bar_lds();
+  }
+}
+
+// ---------------------------------------------------------------- host side
+
+int persistent_grid(bool mfma);
+
+// Score workspace of the matrix-core path: [shared thresholds, cap x u32]
+// (rounded to 256 bytes) followed by the partial lists.
+size_t mfma_thr_bytes(int64_t cap) { return ((size_t)cap * 4 + 255) & ~(size_t)255; }
+
+// worst case over n_u in [1, cap] and grids up to grid_max of n_u * S * f(k)
+static size_t mfma_split_worst(int64_t cap, int64_t N, int k, int grid_max, size_t per_slice) {
+  size_t best = 0;
+  const int64_t qtmax = (cap + kMMQ - 1) / kMMQ;
+  int64_t smax = kMSplitMaxSK / k;
+  if (smax < 1) smax = 1;
+  for (int64_t qt = 1; qt <= qtmax; ++qt) {
+    const int64_t nu = qt * kMMQ < cap ? qt * kMMQ : cap;
+    for (int64_t g = 8; g <= grid_max; g += 8) {
+      const Split sp = make_split(nu, N, kMMQ, kMNC, g, smax);
+      const size_t b = (size_t)nu * (size_t)sp.S * per_slice;
+      if (b > best) best = b;
+    }
+  }
+  return (best + 255) & ~(size_t)255;
+}
+
+// Score workspace of the matrix-core path: [shared thresholds, cap x u32 |
+// seed-pass lane maxima, n_u x S x 8 u32 | partial lists, n_u x S x k keys],
+// each rounded to 256 bytes.
+size_t mfma_lmax_bytes(int64_t cap, int64_t N, int k, int grid_max) {
+  return mfma_split_worst(cap, N, k, grid_max, (size_t)kMLanesQ * 4);
+}
+
+size_t mfma_partial_bytes(int64_t cap, int64_t N, int k, int grid_max) {
+  return mfma_thr_bytes(cap) + mfma_lmax_bytes(cap, N, k, grid_max) +
+         mfma_split_worst(cap, N, k, grid_max, (size_t)k * 8);
+}
+
+// Offset of the partial lists in the score workspace.
+size_t mfma_part_offset(int64_t cap, int64_t N, int k, int grid_max) {
+  return mfma_thr_bytes(cap) + mfma_lmax_bytes(cap, N, k, grid_max);
+}
+
+void mfma_split_params(int *mq, int *nc, int64_t *smax, int k) {
+  *mq = kMMQ;
+  *nc = kMNC;
+  int64_t s = kMSplitMaxSK / k;
+  *smax = s < 1 ? 1 : s;
+}
+
+template <typename K>
+static hipError_t launch_mfma(K kern, int grid, int lds, const MfmaArgs &a, hipStream_t st) {
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(kMT), lds, st, a);
+  return hipGetLastError();
+}
+
+__global__ void mfma_gthr_init(uint32_t *g, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) g[i] = 0u;
+}
+
+// Threshold seed per distinct query: the k-th largest of its lane maxima
+// from the seed pass (at most kSeedMax of them), written to gthr.
+constexpr int kSeedMax = 8192;
+constexpr int kSeedThreads = 1024;
+__global__ __launch_bounds__(kSeedThreads) void mfma_seed_kernel(
+    const uint32_t *__restrict__ lmax, int64_t n_unique, const int64_t *__restrict__ nu_dev,
+    int64_t cap, int64_t N, int k, int64_t smax, int grid, uint32_t *__restrict__ gthr) {
+  __shared__ uint32_t buf[kSeedMax];
+  const int64_t nu = read_nu(n_unique, nu_dev, cap);
+  const Split sp = make_split(nu, N, kMMQ, kMNC, grid, smax);
+  const int64_t per = sp.S * kMLanesQ;
+  const int n = (int)(per < kSeedMax ? per : kSeedMax);
+  if (n < k) return;   // fewer lane maxima than k: no seed
+  int P = 1;
+  while (P < n) P <<= 1;
+  const int tid = threadIdx.x;
+  for (int64_t q = blockIdx.x; q < nu; q += gridDim.x) {
+    const uint32_t *src = lmax + q * per;
+    for (int i = tid; i < P; i += kSeedThreads) buf[i] = i < n ? src[i] : 0u;
+    __syncthreads();
+    for (int size = 2; size <= P; size <<= 1) {
+      for (int stride = size >> 1; stride > 0; stride >>= 1) {
+        for (int t = tid; t < (P >> 1); t += kSeedThreads) {
+          const int i = 2 * t - (t & (stride - 1));
+          const int j = i + stride;
+          const bool desc = (i & size) == 0;
+          const uint32_t x = buf[i], y = buf[j];
+          if ((x < y) == desc) {
+            buf[i] = y;
+            buf[j] = x;
+          }
+        }
+        __syncthreads();
+      }
+    }
+    if (tid == 0 && buf[k - 1]) gthr[q] = buf[k - 1];
+    __syncthreads();
+  }
+}
+
+hipError_t launch_score_mfma(const void *q, const void *corpus, const float *scale, int64_t N,
+                             int64_t d, int k, int64_t n_unique, const int64_t *nu_dev,
+                             int64_t cap, bool fp8, void *ws, hipStream_t st) {
+  // shared thresholds start empty on every call (a fill kernel, so that the
+  // sequence can be captured in a graph)
+  uint32_t *gthr = (uint32_t *)ws;
+  uint32_t *lmax = (uint32_t *)((unsigned char *)ws + mfma_thr_bytes(cap));
+  void *part = (unsigned char *)ws + mfma_part_offset(cap, N, k, kMGridMax);
+  if (cap > 0) {
+    hipLaunchKernelGGL(mfma_gthr_init, dim3((unsigned)((cap + 255) / 256)), dim3(256), 0, st,
+                       gthr, cap);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  MfmaArgs a;
+  a.q = q;
+  a.corpus = corpus;
+  a.scale = scale;
+  a.N = N;
+  a.d = d;
+  a.k = k;
+  a.n_unique = n_unique;
+  a.n_unique_dev = nu_dev;
+  a.cap = cap;
+  a.part = (uint64_t *)part;
+  a.gthr = gthr;
+  a.lmax = lmax;
+  a.grid = persistent_grid(true);
+  // k-lists in LDS when they fit beside the ring
+  const bool ll = mfma_lds_bytes(fp8, true, k) <= kMLdsMax;
+  const int lds = mfma_lds_bytes(fp8, ll, k);
+  const int lds_seed = mfma_lds_bytes(fp8, false, k);
+  auto run = [&](bool seed) {
+    if (seed) return fp8 ? launch_mfma(score_mfma_dma<true, false, true>, a.grid, lds_seed, a, st)
+                         : launch_mfma(score_mfma_dma<false, false, true>, a.grid, lds_seed, a, st);
+    if (fp8) return ll ? launch_mfma(score_mfma_dma<true, true, false>, a.grid, lds, a, st)
+                       : launch_mfma(score_mfma_dma<true, false, false>, a.grid, lds, a, st);
+    return ll ? launch_mfma(score_mfma_dma<false, true, false>, a.grid, lds, a, st)
+              : launch_mfma(score_mfma_dma<false, false, false>, a.grid, lds, a, st);
+  };
+  // Seed pass: score the first tile of every slice and keep only lane
+  // maxima; their k-th largest per query (a lower bound of the query's k-th
+  // best over the corpus, taken over a sample of S tiles spread over it)
+  // seeds the shared thresholds.  The main pass then scores every tile with
+  // lists that stay nearly untouched from the first tile on.
+  hipError_t e = run(true);
+  if (e != hipSuccess) return e;
+  if (cap > 0) {
+    int64_t smax = kMSplitMaxSK / k;
+    if (smax < 1) smax = 1;
+    const int64_t blocks = (n_unique >= 0 ? n_unique : cap) < 65535 ? (n_unique >= 0 ? n_unique : cap) : 65535;
+    if (blocks > 0) {
+      hipLaunchKernelGGL(mfma_seed_kernel, dim3((unsigned)blocks), dim3(kSeedThreads), 0, st,
+                         a.lmax, n_unique, nu_dev, cap, N, k, smax, a.grid, gthr);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+  }
+  return run(false);
+}
+
+}  // namespace hs
