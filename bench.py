@@ -31,7 +31,7 @@ sys.path.insert(0, ROOT)
 METRIC = "merged retrieval queries/s + achieved HBM GB/s or MFMA % (dedup+score+top-k)"
 PEAK_HBM_GBS = 8000.0
 PEAK_MFMA = {"bf16": 2500.0}          # dense TFLOP/s (no sparsity)
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_partial_ridge1m_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_step_ridge1m_traffic.json")
 KERNEL_SOURCES = ["paper_2607_22578_amd/csrc/score_mfma.hip", "paper_2607_22578_amd/csrc/score.hip",
                   "paper_2607_22578_amd/csrc/common.h"]
 # The score step (hs_score_partial) is four launches on one stream: the

@@ -1,0 +1,65 @@
+"""Matrix-core scoring path on shapes away from the workload sizes, against
+the oracle (acceptance rule of oracle/accept.py): dimensions that leave a
+partial last K stage (the copies read zeros past d), corpora smaller than
+one 384-row tile or with a ragged last tile, k-lists held in global memory
+instead of LDS, and k too large for the first-pass threshold seed."""
+import numpy as np
+import pytest
+
+import synth
+from gpu_harness import check_dedup, check_delivery, check_unique_topk, note, run_merge
+
+pytestmark = pytest.mark.gpu
+
+
+def _stream(n_corpus: int, d: int, enc: str):
+    """The 1M-row workload's request stream (329 distinct queries over 2,048
+    requests) with query rows of width d and a fresh corpus of n_corpus rows
+    in storage encoding `enc`."""
+    w = synth.make("ridge1m", n_corpus=1, with_corpus=False)
+    q, _ = synth.gaussian_rows(w.seed, synth.S_QUERY, 0, d, "bf16", row_ids=w.template_ids)
+    c, sc = synth.gaussian_rows(w.seed, synth.S_CORPUS, n_corpus, d, enc)
+    return w, q, c, sc
+
+
+@pytest.mark.parametrize("d,n_corpus", [(8, 1000), (40, 385), (200, 2000), (776, 1500)])
+def test_bf16_partial_stage_and_ragged_tiles(d, n_corpus):
+    w, q, c, _ = _stream(n_corpus, d, "bf16")
+    note(f"bf16 d={d} N={n_corpus}")
+    m = run_merge(w.keys, q, c, 10)
+    ref = check_dedup(m, w.keys)
+    check_unique_topk(m, ref, q, c, 10)
+    check_delivery(m, w.R)
+
+
+@pytest.mark.parametrize("d,n_corpus", [(16, 700), (784, 2500)])
+def test_fp8_partial_stage(d, n_corpus):
+    w, q, c, sc = _stream(n_corpus, d, "fp8")
+    note(f"fp8 d={d} N={n_corpus}")
+    m = run_merge(w.keys, q, c, 10, scale=sc)
+    ref = check_dedup(m, w.keys)
+    check_unique_topk(m, ref, q, c, 10, scale=sc)
+    check_delivery(m, w.R)
+
+
+@pytest.mark.parametrize("k", [19, 20, 64])
+def test_lists_in_lds_and_global(k):
+    # with d = 768 bf16, k-lists fit in LDS up to k = 19 and live in the
+    # partial buffer in global memory from k = 20 on
+    w, q, c, _ = _stream(6000, 768, "bf16")
+    note(f"bf16 k={k}")
+    m = run_merge(w.keys, q, c, k)
+    ref = check_dedup(m, w.keys)
+    check_unique_topk(m, ref, q, c, k)
+    check_delivery(m, w.R)
+
+
+def test_k_beyond_seed():
+    # 1,100 rows are three tiles, so the first pass sees at most 8 * 3 lane
+    # maxima per query: fewer than k, and no threshold seed is written
+    w, q, c, _ = _stream(1100, 128, "bf16")
+    k = 300
+    m = run_merge(w.keys, q, c, k)
+    ref = check_dedup(m, w.keys)
+    check_unique_topk(m, ref, q, c, k)
+    check_delivery(m, w.R)
