@@ -14,7 +14,8 @@
 // scanned by one thread that keeps the query's k best (score, row) keys of
 // this slice.
 // Phase 2 (topk_merge_kernel): per query, the S slice lists (S*k keys) are
-// sorted and the first k are written out.
+// filtered (empty keys, and keys below the query's shared threshold on the
+// matrix-core path), the rest sorted and the first k written out.
 //
 // Result keys order by (score desc, row asc), so ties always go to the lower
 // corpus row, independently of which slice or lane saw them.
@@ -228,30 +229,50 @@ __global__ __launch_bounds__(kThreads) void score_partial_valu(ScoreArgs a) {
 
 constexpr int kMergeThreads = 1024;
 
-// One workgroup per distinct query: bitonic sort (descending) of its S*k
-// slice keys, first k decoded to (score, row).
+// One workgroup per distinct query.  Its S*k slice keys are compacted into
+// LDS, dropping empty keys and, when a shared threshold is given, keys whose
+// score is below it (a lower bound of the query's k-th best score, so every
+// key of the final k survives); the survivors are sorted (bitonic,
+// descending) and the first k decoded to (score, row), ranks past the
+// survivors padded with (-inf, -1).
 __global__ __launch_bounds__(kMergeThreads) void topk_merge_kernel(
-    const uint64_t *__restrict__ part, int64_t n_unique, const int64_t *__restrict__ n_unique_dev,
-    int64_t cap, int64_t N, int k, int mq, int nc, int64_t smax, int grid,
-    float *__restrict__ out_s, int32_t *__restrict__ out_i) {
+    const uint64_t *__restrict__ part, const uint32_t *__restrict__ thr, int64_t n_unique,
+    const int64_t *__restrict__ n_unique_dev, int64_t cap, int64_t N, int k, int mq, int nc,
+    int64_t smax, int grid, float *__restrict__ out_s, int32_t *__restrict__ out_i) {
   __shared__ uint64_t buf[kMaxSK];
+  __shared__ int count;
   const int64_t nu = read_nu(n_unique, n_unique_dev, cap);
   const Split sp = make_split(nu, N, mq, nc, grid, smax);
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int n = (int)(sp.S * k);
   for (int64_t q = blockIdx.x; q < nu; q += gridDim.x) {
-    const int n = (int)(sp.S * k);
-    int P = 2;
-    while (P < n) P <<= 1;
+    const uint32_t t = thr ? thr[q] : 0u;
     const uint64_t *src = part + q * sp.S * k;
-    for (int i = tid; i < P; i += kMergeThreads) buf[i] = i < n ? src[i] : 0ull;
+    if (tid == 0) count = 0;
+    __syncthreads();
+    for (int i0 = 0; i0 < n; i0 += kMergeThreads) {
+      const int i = i0 + tid;
+      const uint64_t key = i < n ? src[i] : 0ull;
+      const bool keep = key != 0ull && (uint32_t)(key >> 32) >= t;
+      const uint64_t mask = __builtin_amdgcn_ballot_w64(keep);
+      int base = 0;
+      if (lane == 0 && mask) base = atomicAdd(&count, __popcll(mask));
+      base = __shfl(base, 0);
+      if (keep) buf[base + __popcll(mask & ((1ull << lane) - 1ull))] = key;
+    }
+    __syncthreads();
+    const int m = count;
+    int P = 2;
+    while (P < m) P <<= 1;
+    for (int i = m + tid; i < P; i += kMergeThreads) buf[i] = 0ull;
     __syncthreads();
     for (int size = 2; size <= P; size <<= 1) {
       for (int stride = size >> 1; stride > 0; stride >>= 1) {
-        for (int t = tid; t < (P >> 1); t += kMergeThreads) {
-          int i = 2 * t - (t & (stride - 1));
-          int j = i + stride;
-          bool desc = (i & size) == 0;
-          uint64_t x = buf[i], y = buf[j];
+        for (int u = tid; u < (P >> 1); u += kMergeThreads) {
+          const int i = 2 * u - (u & (stride - 1));
+          const int j = i + stride;
+          const bool desc = (i & size) == 0;
+          const uint64_t x = buf[i], y = buf[j];
           if ((x < y) == desc) {
             buf[i] = y;
             buf[j] = x;
@@ -263,7 +284,7 @@ __global__ __launch_bounds__(kMergeThreads) void topk_merge_kernel(
     for (int j = tid; j < k; j += kMergeThreads) {
       float sc;
       int32_t row;
-      decode_key(j < P ? buf[j] : 0ull, sc, row);
+      decode_key(j < m ? buf[j] : 0ull, sc, row);
       out_s[q * k + j] = sc;
       out_i[q * k + j] = row;
     }
@@ -367,13 +388,18 @@ hipError_t launch_topk_merge(const void *part, int64_t n_unique, const int64_t *
   int mq = kVMQ, nc = kVNC;
   int64_t smax = kMaxSK / k;
   if (smax < 1) smax = 1;
+  const uint32_t *thr = nullptr;
   if (!valu) {
     mfma_split_params(&mq, &nc, &smax, k);
-    // the matrix-core path keeps its partial lists after its other scratch
+    // the matrix-core path starts its workspace with the shared thresholds
+    // and keeps its partial lists after its other scratch
+    thr = (const uint32_t *)part;
     part = (const unsigned char *)part + mfma_part_offset(cap, N, k, kGridMax);
   }
+  // a persistent grid of at most two workgroups per CU loops over queries
+  if (blocks > 2 * (int64_t)grid) blocks = 2 * (int64_t)grid;
   hipLaunchKernelGGL(topk_merge_kernel, dim3((unsigned)blocks), dim3(kMergeThreads), 0, st,
-                     (const uint64_t *)part, n_unique, nu_dev, cap, N, k, mq, nc, smax, grid,
+                     (const uint64_t *)part, thr, n_unique, nu_dev, cap, N, k, mq, nc, smax, grid,
                      out_s, out_i);
   return hipGetLastError();
 }

@@ -409,34 +409,60 @@ __device__ __forceinline__ int opaque(int x) {
   return x;
 }
 
-// Score of accumulator element (rb, qb, i) of this lane: fp8 row scale applied,
-// NaN for rows past N (NaN fails every >= test and fmaxf ignores it).  `lim`
-// = number of valid rows of the tile counted from this lane's first row.
+// Turns the tile's accumulators into scores in place, once per tile: the fp8
+// row scale applied, NaN for rows past N (NaN fails every >= test and fmaxf
+// ignores it).  Accumulator element (rb, qb, i) of a lane is row
+// rb * 32 + 8 * (i / 4) + i % 4 counted from the lane's first row; `lim0` =
+// number of valid rows from there.  Everything after reads the accumulators
+// directly.
 template <bool FP8>
-__device__ __forceinline__ float mscore(const f32x16m (&acc)[kMRB][kMQB], const float *ssc_lane,
-                                        int lim, int rb, int qb, int i) {
-  const int r = rb * 32 + 8 * (i >> 2) + (i & 3);
-  float v = acc[rb][qb][i];
-  if constexpr (FP8) v *= ssc_lane[r];
-  return r < lim ? v : __builtin_nanf("");
+__device__ __forceinline__ void finish_scores(f32x16m (&acc)[kMRB][kMQB], const float *ssc_lane,
+                                              int lim0) {
+  if constexpr (FP8) {
+#pragma unroll
+    for (int rb = 0; rb < kMRB; ++rb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        // (an opaque offset keeps the compiler from loading all 48 scales
+        // ahead of the multiplies)
+        const float4 s4 = *reinterpret_cast<const float4 *>(ssc_lane + opaque(rb * 32 + 8 * j));
+#pragma unroll
+        for (int qb = 0; qb < kMQB; ++qb) {
+          acc[rb][qb][4 * j + 0] *= s4.x;
+          acc[rb][qb][4 * j + 1] *= s4.y;
+          acc[rb][qb][4 * j + 2] *= s4.z;
+          acc[rb][qb][4 * j + 3] *= s4.w;
+          asm volatile("" : "+a"(acc[rb][qb]));
+        }
+      }
+  }
+  if (lim0 < 32 * kMRB) {   // some of this lane's rows are past N
+    const float nan = __builtin_nanf("");
+#pragma unroll
+    for (int rb = 0; rb < kMRB; ++rb)
+#pragma unroll
+      for (int qb = 0; qb < kMQB; ++qb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (rb * 32 + 8 * (i >> 2) + (i & 3) >= lim0) acc[rb][qb][i] = nan;
+    pin_acc(acc);
+  }
 }
 
 // Warm-up: per query, the smallest of this lane's group maxima (groups of
 // SPAN consecutive scores), combined over the two lane halves and stored per
 // wave.
-template <bool FP8, int SPAN>
-__device__ __forceinline__ void warm_minima(const MLds &L, f32x16m (&acc)[kMRB][kMQB],
-                                            const float *ssc_lane, int lim0, int wv, int c,
-                                            int h) {
+template <int SPAN>
+__device__ __forceinline__ void warm_minima(const MLds &L, f32x16m (&acc)[kMRB][kMQB], int wv,
+                                            int c, int h) {
 #pragma unroll
   for (int qb = 0; qb < kMQB; ++qb) {
-    const int lim = opaque(lim0);
     float mn = __builtin_inff(), m = -__builtin_inff();
 #pragma unroll
     for (int rb = 0; rb < kMRB; ++rb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        m = fmaxf(m, mscore<FP8>(acc, ssc_lane, lim, rb, qb, i));
+        m = fmaxf(m, acc[rb][qb][i]);
         if ((rb * 16 + i + 1) % SPAN == 0) {
           mn = fminf(mn, m);
           m = -__builtin_inff();
@@ -461,16 +487,15 @@ __device__ __forceinline__ void mtile_lane_maxima(const MfmaArgs &a, const MItem
   const int lrow = wv * 32 * kMRB + 4 * h;
   const int lim0 = (int)a.N - row0 - lrow;
   const float *ssc_lane = FP8 ? ssc + lrow : nullptr;
-  bar_lds();   // the tile's row scales are in LDS for every wave
   pin_acc(acc);
+  finish_scores<FP8>(acc, ssc_lane, lim0);
 #pragma unroll
   for (int qb = 0; qb < kMQB; ++qb) {
-    const int lim = opaque(lim0);
     float m = -__builtin_inff();
 #pragma unroll
     for (int rb = 0; rb < kMRB; ++rb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) m = fmaxf(m, mscore<FP8>(acc, ssc_lane, lim, rb, qb, i));
+      for (int i = 0; i < 16; ++i) m = fmaxf(m, acc[rb][qb][i]);
     const int ql = qb * 32 + c;
     if (ql < it.qvalid)
       a.lmax[((int64_t)(it.qbase + ql) * it.S + it.s) * kMLanesQ + wv * 2 + h] =
@@ -493,19 +518,20 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
   const int lim0 = (int)a.N - row0 - lrow;
   const float *ssc_lane = FP8 ? ssc + lrow : nullptr;
   pin_acc(acc);
+  finish_scores<FP8>(acc, ssc_lane, lim0);
   const int gpl = mwarm_groups(a.k);
   if (first && gpl > 0) {
     // warm-up threshold: the smallest of kMLanesQ * gpl group maxima (the
     // queue, which these minima alias, is empty at an item's first tile)
     bar_lds();
     switch (gpl) {
-      case 1: warm_minima<FP8, kMVals / 1>(L, acc, ssc_lane, lim0, wv, c, h); break;
-      case 2: warm_minima<FP8, kMVals / 2>(L, acc, ssc_lane, lim0, wv, c, h); break;
-      case 4: warm_minima<FP8, kMVals / 4>(L, acc, ssc_lane, lim0, wv, c, h); break;
-      case 8: warm_minima<FP8, kMVals / 8>(L, acc, ssc_lane, lim0, wv, c, h); break;
-      case 16: warm_minima<FP8, kMVals / 16>(L, acc, ssc_lane, lim0, wv, c, h); break;
-      case 32: warm_minima<FP8, kMVals / 32>(L, acc, ssc_lane, lim0, wv, c, h); break;
-      default: warm_minima<FP8, 1>(L, acc, ssc_lane, lim0, wv, c, h); break;
+      case 1: warm_minima<kMVals / 1>(L, acc, wv, c, h); break;
+      case 2: warm_minima<kMVals / 2>(L, acc, wv, c, h); break;
+      case 4: warm_minima<kMVals / 4>(L, acc, wv, c, h); break;
+      case 8: warm_minima<kMVals / 8>(L, acc, wv, c, h); break;
+      case 16: warm_minima<kMVals / 16>(L, acc, wv, c, h); break;
+      case 32: warm_minima<kMVals / 32>(L, acc, wv, c, h); break;
+      default: warm_minima<1>(L, acc, wv, c, h); break;
     }
     bar_lds();
     if (tid < it.qvalid) {
@@ -534,10 +560,8 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
   // half blocks of this lane whose best score reaches the query threshold
   pin_acc(acc);
   uint64_t pend[kMQB];
-  const bool tail = lim0 < 32 * kMRB;   // some of this lane's rows may be past N
 #pragma unroll
   for (int qb = 0; qb < kMQB; ++qb) {
-    const int lim = opaque(lim0);
     const float th = thr_r[qb];
     uint64_t p = 0;
 #pragma unroll
@@ -546,8 +570,7 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int i = 8 * (hb & 1) + j;
-        m = fmaxf(m, (!FP8 && !tail) ? acc[hb >> 1][qb][i]
-                                     : mscore<FP8>(acc, ssc_lane, lim, hb >> 1, qb, i));
+        m = fmaxf(m, acc[hb >> 1][qb][i]);
       }
       p |= m >= th ? 0xFFull << (8 * hb) : 0ull;
     }
@@ -567,7 +590,6 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
       if (!__builtin_amdgcn_ballot_w64(pend[qb] != 0)) continue;
       const int ql = qb * 32 + c;
       const float th = thr_r[qb];
-      const int lim = opaque(lim0);
       const int rowb = opaque(row0 + lrow);
       uint64_t keep = 0;
 #pragma unroll
@@ -580,8 +602,7 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
         uint32_t cand = 0;
 #pragma unroll
         for (int jj = 0; jj < 8; ++jj) {
-          v[jj] = (!FP8 && !tail) ? acc[rb][qb][8 * half + jj]
-                                  : mscore<FP8>(acc, ssc_lane, lim, rb, qb, 8 * half + jj);
+          v[jj] = acc[rb][qb][8 * half + jj];
           cand |= ((m8 >> jj) & 1u) && v[jj] >= th ? 1u << jj : 0u;
         }
         if (!__builtin_amdgcn_ballot_w64(cand != 0)) continue;
@@ -733,14 +754,17 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
       i_slot = i_slot + 1 == G::ns ? 0 : i_slot + 1;
       --i_left;
     };
+    // vector-memory operations issued after the copies of stage y, up to
+    // the call that copied stage z (tile-first extras not counted: waiting
+    // for fewer outstanding operations only waits longer)
+    auto younger_ops = [&](int y, int z) __attribute__((always_inline)) {
+      return z > y ? (z - y) * G::ldma : 0;
+    };
 
 #pragma unroll
     for (int j = 0; j < G::ns; ++j) issue();
-    // chunk 0 landed (younger copies: chunks 1 .. ns-1, at most T-1 of them)
-    {
-      const int younger = T - 1 < G::ns - 1 ? T - 1 : G::ns - 1;
-      wait_vm(younger > 0 ? younger * G::ldma : 0);
-    }
+    // chunk 0 landed (calls for chunks 1 .. ns-1 are younger)
+    wait_vm(younger_ops(0, (T < G::ns ? T : G::ns) - 1));
     bar_lds();
 
 #pragma unroll
@@ -752,7 +776,11 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
 
     // one stage: two halves of two MFMA steps each; the second half carries
     // the wait for the next stage, the barrier, the next copies and the
-    // next stage's first fragments, so that reads overlap the last MFMAs
+    // next stage's first fragments, so that reads overlap the last MFMAs.
+    // (Issuing the copies earlier, right after the slot's last reads, gives
+    // them more time but costs a second barrier per stage, which was slower:
+    // the loop is bound by the matrix cores sharing the CU with the LDS
+    // reads more than by copy latency.)
     auto stage = [&](auto first_c, bool rd) __attribute__((always_inline)) {
       constexpr bool FIRST = decltype(first_c)::value;
       mfma_step<FP8, FIRST>(acc, f0, 0);
@@ -761,9 +789,8 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
       mfma_step<FP8, false>(acc, f1, 0);
       r_slot = r_slot + 1 == G::ns ? 0 : r_slot + 1;
       if (g + 1 < T) {
-        // stage g+1 landed: younger copies are those of stages g+2 .. g+ns-1
-        const int younger = T - 2 - g < G::ns - 2 ? T - 2 - g : G::ns - 2;
-        wait_vm(younger > 0 ? younger * G::ldma : 0);
+        // stage g+1 landed: younger calls are those of stages g+2 .. g+ns-1
+        wait_vm(younger_ops(g + 1, g + G::ns - 1 < T - 1 ? g + G::ns - 1 : T - 1));
         bar_lds();
         issue();   // stage g+ns into the slot stage g used
       }
@@ -873,41 +900,74 @@ __global__ void mfma_gthr_init(uint32_t *g, int64_t n) {
 }
 
 // Threshold seed per distinct query: the k-th largest of its lane maxima
-// from the seed pass (at most kSeedMax of them), written to gthr.
+// from the seed pass (at most kSeedMax of them), written to gthr.  Radix
+// select on the 32-bit ordered scores, 8 bits per pass: a pass counts the
+// values that carry the digits chosen so far by their next digit, and keeps
+// the largest digit whose count of values at or above it reaches the rank
+// still sought.
 constexpr int kSeedMax = 8192;
-constexpr int kSeedThreads = 1024;
+constexpr int kSeedThreads = 256;
 __global__ __launch_bounds__(kSeedThreads) void mfma_seed_kernel(
     const uint32_t *__restrict__ lmax, int64_t n_unique, const int64_t *__restrict__ nu_dev,
     int64_t cap, int64_t N, int k, int64_t smax, int grid, uint32_t *__restrict__ gthr) {
-  __shared__ uint32_t buf[kSeedMax];
+  __shared__ uint32_t vals[kSeedMax];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t sel[2];   // chosen digit, values above it
   const int64_t nu = read_nu(n_unique, nu_dev, cap);
   const Split sp = make_split(nu, N, kMMQ, kMNC, grid, smax);
   const int64_t per = sp.S * kMLanesQ;
   const int n = (int)(per < kSeedMax ? per : kSeedMax);
   if (n < k) return;   // fewer lane maxima than k: no seed
-  int P = 1;
-  while (P < n) P <<= 1;
   const int tid = threadIdx.x;
   for (int64_t q = blockIdx.x; q < nu; q += gridDim.x) {
     const uint32_t *src = lmax + q * per;
-    for (int i = tid; i < P; i += kSeedThreads) buf[i] = i < n ? src[i] : 0u;
-    __syncthreads();
-    for (int size = 2; size <= P; size <<= 1) {
-      for (int stride = size >> 1; stride > 0; stride >>= 1) {
-        for (int t = tid; t < (P >> 1); t += kSeedThreads) {
-          const int i = 2 * t - (t & (stride - 1));
-          const int j = i + stride;
-          const bool desc = (i & size) == 0;
-          const uint32_t x = buf[i], y = buf[j];
-          if ((x < y) == desc) {
-            buf[i] = y;
-            buf[j] = x;
+    for (int i = tid; i < n; i += kSeedThreads) vals[i] = src[i];
+    uint32_t prefix = 0u, pmask = 0u;
+    int kk = k;   // rank sought among the values that carry prefix
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      hist[tid] = 0u;
+      __syncthreads();
+      for (int i = tid; i < n; i += kSeedThreads) {
+        const uint32_t v = vals[i];
+        if ((v & pmask) == prefix) atomicAdd(&hist[(v >> shift) & 0xFFu], 1u);
+      }
+      __syncthreads();
+      if (tid < kWave) {
+        // lane l holds digits 255 - 4l - j (j = 0..3), largest first; an
+        // exclusive scan over lanes counts the values above its digits
+        uint32_t c[4], sum = 0u;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          c[j] = hist[255 - 4 * tid - j];
+          sum += c[j];
+        }
+        uint32_t incl = sum;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+          const uint32_t t = __shfl_up(incl, o);
+          if (tid >= o) incl += t;
+        }
+        uint32_t above = incl - sum;
+        if (above < (uint32_t)kk && (uint32_t)kk <= incl) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            if (above + c[j] >= (uint32_t)kk) {
+              sel[0] = 255u - 4u * tid - j;
+              sel[1] = above;
+              break;
+            }
+            above += c[j];
           }
         }
-        __syncthreads();
       }
+      __syncthreads();
+      prefix |= sel[0] << shift;
+      pmask |= 0xFFu << shift;
+      kk -= (int)sel[1];
+      // (hist was last read before the barrier above; sel is rewritten only
+      // after the next pass's counting barrier)
     }
-    if (tid == 0 && buf[k - 1]) gthr[q] = buf[k - 1];
+    if (tid == 0 && prefix) gthr[q] = prefix;
     __syncthreads();
   }
 }
@@ -962,7 +1022,8 @@ hipError_t launch_score_mfma(const void *q, const void *corpus, const float *sca
   if (cap > 0) {
     int64_t smax = kMSplitMaxSK / k;
     if (smax < 1) smax = 1;
-    const int64_t blocks = (n_unique >= 0 ? n_unique : cap) < 65535 ? (n_unique >= 0 ? n_unique : cap) : 65535;
+    const int64_t want = n_unique >= 0 ? n_unique : cap;
+    const int64_t blocks = want < 4 * (int64_t)a.grid ? want : 4 * (int64_t)a.grid;
     if (blocks > 0) {
       hipLaunchKernelGGL(mfma_seed_kernel, dim3((unsigned)blocks), dim3(kSeedThreads), 0, st,
                          a.lmax, n_unique, nu_dev, cap, N, k, smax, a.grid, gthr);

@@ -42,10 +42,10 @@ def test_fp8_partial_stage(d, n_corpus):
     check_delivery(m, w.R)
 
 
-@pytest.mark.parametrize("k", [19, 20, 64])
+@pytest.mark.parametrize("k", [18, 19, 64])
 def test_lists_in_lds_and_global(k):
-    # with d = 768 bf16, k-lists fit in LDS up to k = 19 and live in the
-    # partial buffer in global memory from k = 20 on
+    # with a bf16 corpus, k-lists fit in LDS up to k = 18 and live in the
+    # partial buffer in global memory from k = 19 on
     w, q, c, _ = _stream(6000, 768, "bf16")
     note(f"bf16 k={k}")
     m = run_merge(w.keys, q, c, k)
