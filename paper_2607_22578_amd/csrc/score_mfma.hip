@@ -556,76 +556,83 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
     g_r[qb] = gq ? unord_score(gq) : -__builtin_inff();
     thr_r[qb] = fmaxf(thr_r[qb], g_r[qb]);
   }
-  // scores still to examine, 8 per byte (half of a 32-row block): the
-  // half blocks of this lane whose best score reaches the query threshold
+  // Screening: elig[qb] bit 16 rb + i marks score (rb, qb, i) of this lane
+  // as still to be examined; a 16-score row block is eligible when its best
+  // score reaches the query threshold.
   pin_acc(acc);
-  uint64_t pend[kMQB];
+  uint64_t elig[kMQB];
 #pragma unroll
   for (int qb = 0; qb < kMQB; ++qb) {
     const float th = thr_r[qb];
-    uint64_t p = 0;
+    uint64_t e = 0;
 #pragma unroll
-    for (int hb = 0; hb < 2 * kMRB; ++hb) {
+    for (int rb = 0; rb < kMRB; ++rb) {
       float m = ninf;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int i = 8 * (hb & 1) + j;
-        m = fmaxf(m, acc[hb >> 1][qb][i]);
-      }
-      p |= m >= th ? 0xFFull << (8 * hb) : 0ull;
+      for (int i = 0; i < 16; ++i) m = fmaxf(m, acc[rb][qb][i]);
+      e |= m >= th ? 0xFFFFull << (16 * rb) : 0ull;
     }
-    pend[qb] = qb * 32 + c < it.qvalid ? p : 0ull;
+    elig[qb] = qb * 32 + c < it.qvalid ? e : 0ull;
   }
   // Scores at or above the current threshold are appended to the per-query
   // LDS queues (atomics, no barrier).  Merges into the k-lists are deferred:
   // one barrier per tile checks whether some queue overflowed (its
-  // candidates stay pending) or is half full; only then do the threads of
-  // the queries merge, the thresholds rise, and pending candidates are
-  // examined again.
+  // candidates stay eligible) or is half full; only then do the threads of
+  // the queries merge, the thresholds rise, and the candidates left over
+  // are examined again.
   for (;;) {
     bool ovf = false, full = false;
     pin_acc(acc);
 #pragma unroll
     for (int qb = 0; qb < kMQB; ++qb) {
-      if (!__builtin_amdgcn_ballot_w64(pend[qb] != 0)) continue;
       const int ql = qb * 32 + c;
       const float th = thr_r[qb];
-      const int rowb = opaque(row0 + lrow);
-      uint64_t keep = 0;
+      uint64_t fail = 0;
 #pragma unroll
-      for (int hb = 0; hb < 2 * kMRB; ++hb) {
-        const int rb = hb >> 1, half = hb & 1;
-        const uint32_t m8 = (uint32_t)(pend[qb] >> (8 * hb)) & 0xFFu;
-        if (!__builtin_amdgcn_ballot_w64(m8 != 0)) continue;
-        // exact candidates of this half block under the current threshold
-        float v[8];
+      for (int rb = 0; rb < kMRB; ++rb) {
+        const uint32_t el = (uint32_t)(elig[qb] >> (16 * rb)) & 0xFFFFu;
+        if (!__builtin_amdgcn_ballot_w64(el != 0)) continue;
+        float v[16];
         uint32_t cand = 0;
 #pragma unroll
-        for (int jj = 0; jj < 8; ++jj) {
-          v[jj] = acc[rb][qb][8 * half + jj];
-          cand |= ((m8 >> jj) & 1u) && v[jj] >= th ? 1u << jj : 0u;
+        for (int i = 0; i < 16; ++i) {
+          v[i] = acc[rb][qb][i];
+          cand |= v[i] >= th ? 1u << i : 0u;
         }
+        cand &= el;
         if (!__builtin_amdgcn_ballot_w64(cand != 0)) continue;
-        uint32_t rest = 0;
+        // one atomic per lane and block reserves queue slots for all its
+        // candidates; the ones past the queue's room stay eligible
+        const int rowb = opaque(row0 + lrow + rb * 32);
+        int slot = 0;
+        if (cand) slot = atomicAdd(&L.qcount[ql], __builtin_popcount(cand));
         while (cand) {
-          const int jx = __builtin_ctz(cand);
-          float sc = v[0];
-#pragma unroll
-          for (int jj = 1; jj < 8; ++jj) sc = jx == jj ? v[jj] : sc;
-          const int slot = atomicAdd(&L.qcount[ql], 1);
           if (slot >= kMQcap) {
-            rest = cand;
+            fail |= (uint64_t)cand << (16 * rb);
             ovf = true;
             break;
           }
-          full |= slot + 1 >= kMQcap / 2;
-          const int r = rb * 32 + 16 * half + 8 * (jx >> 2) + (jx & 3);
-          L.queue[ql * kMQcap + slot] = make_key(sc, (uint32_t)(rowb + r));
+          const int jx = __builtin_ctz(cand);
           cand &= cand - 1u;
+          // v[jx] by a tree of bitwise selects on the bits of jx (opaque
+          // all-ones / zero masks: as plain selects, the compiler turns the
+          // tree into an indexed load from scratch memory)
+          uint32_t w8[8], w4[4];
+          const uint32_t m0 = (uint32_t)opaque(-(jx & 1)), m1 = (uint32_t)opaque(-((jx >> 1) & 1));
+          const uint32_t m2 = (uint32_t)opaque(-((jx >> 2) & 1)), m3 = (uint32_t)opaque(-(jx >> 3));
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+            w8[i] = (__float_as_uint(v[2 * i]) & ~m0) | (__float_as_uint(v[2 * i + 1]) & m0);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) w4[i] = (w8[2 * i] & ~m1) | (w8[2 * i + 1] & m1);
+          const uint32_t w2a = (w4[0] & ~m2) | (w4[1] & m2), w2b = (w4[2] & ~m2) | (w4[3] & m2);
+          const float sc = __uint_as_float((w2a & ~m3) | (w2b & m3));
+          full |= slot + 1 >= kMQcap / 2;
+          L.queue[ql * kMQcap + slot] = make_key(sc, (uint32_t)(rowb + 8 * (jx >> 2) + (jx & 3)));
+          ++slot;
         }
-        keep |= (uint64_t)rest << (8 * hb);
       }
-      pend[qb] = keep;
+      elig[qb] = fail;
     }
     if (__builtin_amdgcn_ballot_w64(ovf) && lane == 0) L.flags[1] = epoch;
     if (__builtin_amdgcn_ballot_w64(full) && lane == 0) L.flags[2] = epoch;
