@@ -105,6 +105,7 @@ __device__ __forceinline__ int swz_slot(int p, int row) {
   return p ^ ((row / (8 / P)) & (P - 1));
 }
 
+constexpr int kMTail = 16;   // list entries kept in LDS when the lists are global
 constexpr int kMWarmBytes = kMW * kMMQ * 4;   // per-wave warm-up minima (alias the queue)
 static_assert(kMWarmBytes <= kMMQ * kMQcap * 8, "warm-up minima fit in the queue");
 
@@ -113,8 +114,17 @@ __host__ __device__ constexpr int mfma_lds_bytes(bool fp8, bool lds_lists, int k
                     Geo<true>::ngt * kMGts * 4
               : Geo<false>::ns * Geo<false>::stage + Geo<false>::ngt * kMGts * 4) +
          kMMQ * kMQcap * 8 + kMMQ * (4 + 4 + 4 + 8 + 4) + 16 +
-         (lds_lists ? kMMQ * k * 8 : 0);
+         (lds_lists ? kMMQ * k * 8 : kMMQ * kMTail * 8);
 }
+// k-lists of up to kMTail entries always fit in LDS, so global lists (which
+// keep kMTail entries in LDS) always have k > kMTail; and the global-list
+// layout fits for every k.
+static_assert(mfma_lds_bytes(false, true, kMTail) <= 160 * 1024 &&
+                  mfma_lds_bytes(true, true, kMTail) <= 160 * 1024,
+              "short k-lists fit in LDS");
+static_assert(mfma_lds_bytes(false, false, 0) <= 160 * 1024 &&
+                  mfma_lds_bytes(true, false, 0) <= 160 * 1024,
+              "global-list layout fits in LDS");
 
 // Warm-up groups per lane and query: the kMVals scores a lane holds for one
 // query are cut into gpl groups so that kMLanesQ * gpl >= k group maxima
@@ -309,6 +319,7 @@ struct MLds {
   float *warm;       // [kMW][MQ] per-wave minima of group maxima (aliases queue)
   int32_t *flags;    // [1] overflow epoch, [2] half-full epoch
   uint64_t *lists;   // [MQ][k] or nullptr (lists in the global partial buffer)
+  uint64_t *tail;    // [MQ][kMTail] last entries of the global lists, or nullptr
 };
 
 template <bool FP8, bool LDS_LISTS>
@@ -328,6 +339,7 @@ __device__ __forceinline__ MLds carve_mlds(unsigned char *p, int k) {
   L.pub = reinterpret_cast<uint32_t *>(p); p += kMMQ * 4;
   L.flags = reinterpret_cast<int32_t *>(p); p += 16;
   L.lists = LDS_LISTS ? reinterpret_cast<uint64_t *>(p) : nullptr;
+  L.tail = LDS_LISTS ? nullptr : reinterpret_cast<uint64_t *>(p);
   (void)k;
   return L;
 }
@@ -359,7 +371,10 @@ __device__ __forceinline__ void publish_thr(const MLds &L, const MfmaArgs &a, co
 // The list is kept sorted in descending key order (empty slots are key 0 at
 // the end), so its minimum is always the last entry and an insertion only
 // shifts the entries it passes: near the threshold, where nearly every
-// entrant lands, that is one or two steps.
+// entrant lands, that is one or two steps.  A list in the global partial
+// buffer keeps its last kMTail entries in LDS while the item runs (its head,
+// positions [0, k - kMTail), stays in global memory): an insertion touches
+// global memory only when its key climbs above that window.
 template <bool LDS_LISTS>
 __device__ __forceinline__ void merge_queue(const MLds &L, const MfmaArgs &a, const MItem &it,
                                             int t) {
@@ -367,21 +382,54 @@ __device__ __forceinline__ void merge_queue(const MLds &L, const MfmaArgs &a, co
   if (cnt <= 0) return;
   const int n = cnt < kMQcap ? cnt : kMQcap;
   const int k = a.k;
-  uint64_t *l = LDS_LISTS ? L.lists + t * k
-                          : a.part + ((int64_t)(it.qbase + t) * it.S + it.s) * k;
   uint64_t mn = L.lmin[t];
-  for (int e = 0; e < n; ++e) {
-    const uint64_t key = L.queue[t * kMQcap + e];
-    if (key > mn) {
-      int i = k - 1;
-      while (i > 0) {
-        const uint64_t prev = l[i - 1];
-        if (prev > key) break;
-        l[i] = prev;
-        --i;
+  if constexpr (LDS_LISTS) {
+    uint64_t *l = L.lists + t * k;
+    for (int e = 0; e < n; ++e) {
+      const uint64_t key = L.queue[t * kMQcap + e];
+      if (key > mn) {
+        int i = k - 1;
+        while (i > 0) {
+          const uint64_t prev = l[i - 1];
+          if (prev > key) break;
+          l[i] = prev;
+          --i;
+        }
+        l[i] = key;
+        mn = l[k - 1];
       }
-      l[i] = key;
-      mn = l[k - 1];
+    }
+  } else {
+    const int hb = k - kMTail;   // first position held in LDS
+    uint64_t *head = a.part + ((int64_t)(it.qbase + t) * it.S + it.s) * k;
+    uint64_t *tl = L.tail + t * kMTail;
+    for (int e = 0; e < n; ++e) {
+      const uint64_t key = L.queue[t * kMQcap + e];
+      if (key > mn) {
+        int i = k - 1;
+        while (i > hb) {
+          const uint64_t prev = tl[i - 1 - hb];
+          if (prev > key) break;
+          tl[i - hb] = prev;
+          --i;
+        }
+        if (i == hb) {
+          while (i > 0) {
+            const uint64_t prev = head[i - 1];
+            if (prev > key) break;
+            if (i == hb)
+              tl[0] = prev;
+            else
+              head[i] = prev;
+            --i;
+          }
+        }
+        if (i >= hb)
+          tl[i - hb] = key;
+        else
+          head[i] = key;
+        mn = tl[kMTail - 1];
+      }
     }
   }
   L.lmin[t] = mn;
@@ -693,9 +741,13 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
       L.lmin[tid] = 0ull;
       L.pub[tid] = 0u;
       if (tid < it.qvalid && !SEED) {
-        uint64_t *l = LDS_LISTS ? L.lists + tid * a.k
-                                : a.part + ((int64_t)(it.qbase + tid) * it.S + it.s) * a.k;
-        for (int j = 0; j < a.k; ++j) l[j] = 0ull;
+        if (LDS_LISTS) {
+          for (int j = 0; j < a.k; ++j) L.lists[tid * a.k + j] = 0ull;
+        } else {
+          uint64_t *l = a.part + ((int64_t)(it.qbase + tid) * it.S + it.s) * a.k;
+          for (int j = 0; j < a.k - kMTail; ++j) l[j] = 0ull;
+          for (int j = 0; j < kMTail; ++j) L.tail[tid * kMTail + j] = 0ull;
+        }
       }
     }
     float thr_r[kMQB];   // (read from L.thr after the prologue barrier)
@@ -704,9 +756,13 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
         make_rsrc((const unsigned char *)a.q + (int64_t)it.qbase * d * 2,
                   (uint32_t)(it.qvalid * d * 2));
 
-    // copy stream: next chunk to issue
+    // copy stream: next chunk to issue.  A chunk is copied in two parts:
+    // issue_a copies the corpus rows of this wave (the only wave that reads
+    // them) and issue_b the wave's share of the query rows, the tile's shared
+    // thresholds and row scales, and advances the stream.  issue_a of a
+    // chunk always precedes its issue_b.
     int i_tl = 0, i_kc = 0, i_slot = 0, i_sc = 0, i_gt = 0, i_left = T;
-    auto issue = [&]() __attribute__((always_inline)) {
+    auto issue_a = [&]() __attribute__((always_inline)) {
       if (i_left <= 0) return;
       const int row0 = (t0 + i_tl) * kMNC;
       const int rows = N - row0 < kMNC ? N - row0 : kMNC;
@@ -717,7 +773,7 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
       const int ln = opaque(lane);
       // corpus copy j: 1 KiB = (64 / PA) rows of G::arow bytes; lane -> (row,
       // slot), and the slot receives the piece that the swizzle puts there
-      constexpr int PA = G::apieces, PB = G::bpieces;
+      constexpr int PA = G::apieces;
       const int arow0 = wv * G::adma * (64 / PA) + ln / PA;
       const uint32_t abase = (uint32_t)(arow0 * d * G::esz +
                                         swz_slot<PA>(ln % PA, ln / PA) * 16 + i_kc * G::esz);
@@ -725,6 +781,12 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
       for (int j = 0; j < G::adma; ++j)
         dma16(ars, st + (wv * G::adma + j) * 1024,
               abase + (uint32_t)(j * (64 / PA) * d * G::esz));
+    };
+    auto issue_b = [&]() __attribute__((always_inline)) {
+      if (i_left <= 0) return;
+      unsigned char *st = L.ring + i_slot * G::stage;
+      const int ln = opaque(lane);
+      constexpr int PB = G::bpieces;
       // query copy j: 1 KiB = (64 / PB) rows; pieces past d read as zeros
       const int bpiece = swz_slot<PB>(ln % PB, ln / PB);
       const bool bok = i_kc + bpiece * 8 < d;
@@ -745,6 +807,8 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
         if (i_kc == 0) {
           // rows [kMRowsW * wv, + 128) of the tile: the wave's own rows and an
           // overlap with the next wave's (same values, same place)
+          const int row0 = (t0 + i_tl) * kMNC;
+          const int rows = N - row0 < kMNC ? N - row0 : kMNC;
           const i32x4m srs = make_rsrc(a.scale + row0, (uint32_t)(rows * 4));
 #pragma unroll
           for (int j = 0; j < 2; ++j)
@@ -761,17 +825,23 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
       i_slot = i_slot + 1 == G::ns ? 0 : i_slot + 1;
       --i_left;
     };
-    // vector-memory operations issued after the copies of stage y, up to
-    // the call that copied stage z (tile-first extras not counted: waiting
-    // for fewer outstanding operations only waits longer)
+    // Vector-memory operations issued after the query part of chunk y, up
+    // to the corpus part of chunk z (only z's corpus part is issued yet).
+    // Tile-first extras are not counted: waiting for fewer outstanding
+    // operations only waits longer.
     auto younger_ops = [&](int y, int z) __attribute__((always_inline)) {
-      return z > y ? (z - y) * G::ldma : 0;
+      int n = 0;
+      for (int x = y + 1; x <= z && x < T; ++x) n += x < z ? G::ldma : G::adma;
+      return n;
     };
 
 #pragma unroll
-    for (int j = 0; j < G::ns; ++j) issue();
-    // chunk 0 landed (calls for chunks 1 .. ns-1 are younger)
-    wait_vm(younger_ops(0, (T < G::ns ? T : G::ns) - 1));
+    for (int j = 0; j < G::ns; ++j) {
+      issue_a();
+      issue_b();
+    }
+    // chunk 0 landed (chunks 1 .. ns-1 are younger)
+    wait_vm(((T < G::ns ? T : G::ns) - 1) * G::ldma);
     bar_lds();
 
 #pragma unroll
@@ -781,25 +851,35 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
     read_frags<FP8>(f0, L.ring, wv, c, h, 0);
     int r_slot = 0, e_sc = 0, e_gt = 0, g = 0;
 
-    // one stage: two halves of two MFMA steps each; the second half carries
-    // the wait for the next stage, the barrier, the next copies and the
-    // next stage's first fragments, so that reads overlap the last MFMAs.
-    // (Issuing the copies earlier, right after the slot's last reads, gives
-    // them more time but costs a second barrier per stage, which was slower:
-    // the loop is bound by the matrix cores sharing the CU with the LDS
-    // reads more than by copy latency.)
+    // One stage: two halves of two MFMA steps each.  Once this wave's reads
+    // of the stage's slot are complete (after step 0) it refills its own
+    // corpus rows there with stage g+ns; no other wave reads them, so no
+    // barrier is needed, and these copies (three quarters of the bytes)
+    // get about half a stage more to arrive.  Before step 3 the wave waits
+    // for stage g+1, the barrier lets every wave's copies of it be read and
+    // lets the query rows of the slot be refilled, and the next stage's
+    // first fragments are read, so that reads overlap the last MFMAs.
+    // (Moving the whole copy earlier costs a second barrier per stage, which
+    // was slower: the loop is bound by the matrix cores sharing the CU with
+    // the LDS reads more than by copy latency.)
     auto stage = [&](auto first_c, bool rd) __attribute__((always_inline)) {
       constexpr bool FIRST = decltype(first_c)::value;
       mfma_step<FP8, FIRST>(acc, f0, 0);
       read_frags<FP8>(f1, L.ring + r_slot * G::stage, wv, c, h, 1);
+      if (i_left > 0) {
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        issue_a();   // this wave's corpus rows of stage g+ns
+      }
       mfma_step<FP8, false>(acc, f0, 1);
       mfma_step<FP8, false>(acc, f1, 0);
       r_slot = r_slot + 1 == G::ns ? 0 : r_slot + 1;
       if (g + 1 < T) {
-        // stage g+1 landed: younger calls are those of stages g+2 .. g+ns-1
-        wait_vm(younger_ops(g + 1, g + G::ns - 1 < T - 1 ? g + G::ns - 1 : T - 1));
+        // stage g+1 landed: younger are the parts of stages g+2 .. g+ns
+        // issued so far
+        wait_vm(younger_ops(g + 1, g + G::ns));
         bar_lds();
-        issue();   // stage g+ns into the slot stage g used
+        issue_b();   // query rows of stage g+ns into the slot stage g used
       }
       pin_step1<FP8>(f1);
       if (rd) read_frags<FP8>(f0, L.ring + r_slot * G::stage, wv, c, h, 0);
@@ -836,6 +916,14 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
       for (int t = tid; t < tot; t += kMT) {
         const int q = t / a.k, j = t - q * a.k;
         a.part[((int64_t)(it.qbase + q) * it.S + it.s) * a.k + j] = L.lists[t];
+      }
+    }
+    if (!LDS_LISTS && !SEED) {
+      bar_lds();
+      const int tot = it.qvalid * kMTail;
+      for (int t = tid; t < tot; t += kMT) {
+        const int q = t / kMTail, j = t - q * kMTail;
+        a.part[((int64_t)(it.qbase + q) * it.S + it.s) * a.k + a.k - kMTail + j] = L.tail[t];
       }
     }
     wait_vm(0);
