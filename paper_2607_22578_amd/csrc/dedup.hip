@@ -7,7 +7,12 @@
 // also makes every output canonical: distinct keys ascending, the survivor of
 // a group is its earliest request, counts[g] = |M(v*)|, inverse[i] = group.
 //
-// Two paths:
+// Three paths:
+//   R <= kHashMax  : one workgroup groups the keys in an LDS hash table
+//                    (first request by atomic min, group size by atomic add),
+//                    orders the distinct keys by counting, for each, the
+//                    distinct keys below it, and maps every request to its
+//                    group through the table;
 //   R <= kSmallMax : one workgroup sorts (key, idx) in LDS with a bitonic
 //                    network and compacts in the same launch;
 //   larger R       : LSD radix sort, 8-bit digits over (key - min) so only
@@ -146,6 +151,113 @@ __global__ __launch_bounds__(kSmallThreads) void dedup_small_kernel(
     }
   }
   if (tid == 0) *nu_out = (int64_t)total;
+}
+
+// ---------------------------------------------------------------- hash path
+
+constexpr int kHashMax = 2048;
+constexpr int kHashSlots = 2 * kHashMax;   // load factor at most 1/2
+constexpr int kHashPer = kHashMax / kSmallThreads;
+
+__global__ __launch_bounds__(kSmallThreads) void dedup_hash_kernel(
+    const int64_t *__restrict__ keys, int R, int64_t *__restrict__ uk, int32_t *__restrict__ fi,
+    int32_t *__restrict__ cnt, int32_t *__restrict__ inv, int64_t *__restrict__ nu_out) {
+  // Mapped keys (map_key: order-preserving to unsigned) in open addressing
+  // with linear probing; mapped value 0 marks an empty slot, so the one key
+  // that maps to 0 (INT64_MIN) is counted in a group of its own (zmin, zcnt).
+  __shared__ unsigned long long hk[kHashSlots];
+  __shared__ int32_t hmin[kHashSlots];   // first request; later the group id
+  __shared__ int32_t hcnt[kHashSlots];
+  __shared__ unsigned long long ck[kHashMax + 8];   // distinct mapped keys
+  __shared__ int32_t cslot[kHashMax + 1];           // their slots (-1: key 0)
+  __shared__ int32_t ncomp, zmin, zcnt, zgroup;
+  const int tid = threadIdx.x;
+  for (int t = tid; t < kHashSlots; t += kSmallThreads) {
+    hk[t] = 0ull;
+    hmin[t] = 0x7FFFFFFF;
+    hcnt[t] = 0;
+  }
+  if (tid == 0) {
+    ncomp = 0;
+    zmin = 0x7FFFFFFF;
+    zcnt = 0;
+  }
+  __syncthreads();
+  int myslot[kHashPer];
+#pragma unroll
+  for (int e = 0; e < kHashPer; ++e) {
+    const int p = tid + e * kSmallThreads;
+    myslot[e] = -1;
+    if (p < R) {
+      const unsigned long long m = map_key(keys[p]);
+      if (m == 0ull) {
+        atomicMin(&zmin, p);
+        atomicAdd(&zcnt, 1);
+      } else {
+        uint32_t sl = (uint32_t)((m * 0x9E3779B97F4A7C15ull) >> 52) & (kHashSlots - 1);
+        for (;;) {   // at most R probes: fewer keys than slots
+          const unsigned long long prev = atomicCAS(&hk[sl], 0ull, m);
+          if (prev == 0ull || prev == m) break;
+          sl = (sl + 1) & (kHashSlots - 1);
+        }
+        atomicMin(&hmin[sl], p);
+        atomicAdd(&hcnt[sl], 1);
+        myslot[e] = (int)sl;
+      }
+    }
+  }
+  __syncthreads();
+  // distinct keys in slot order
+  for (int t = tid; t < kHashSlots; t += kSmallThreads) {
+    if (hk[t] != 0ull) {
+      const int u = atomicAdd(&ncomp, 1);
+      ck[u] = hk[t];
+      cslot[u] = t;
+    }
+  }
+  __syncthreads();
+  if (tid == 0 && zcnt > 0) {
+    ck[ncomp] = 0ull;
+    cslot[ncomp] = -1;
+    ++ncomp;
+  }
+  __syncthreads();
+  const int n = ncomp;
+  // group id = number of distinct keys below (keys are distinct); the list
+  // is padded to a multiple of 8 with all-ones keys (never below a key) so
+  // that eight independent reads are in flight at a time
+  const int n8 = (n + 7) & ~7;
+  for (int u = n + tid; u < n8; u += kSmallThreads) ck[u] = ~0ull;
+  __syncthreads();
+  for (int u = tid; u < n; u += kSmallThreads) {
+    const unsigned long long m = ck[u];
+    int r = 0;
+    for (int j = 0; j < n8; j += 8) {
+      unsigned long long b[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) b[t] = ck[j + t];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) r += b[t] < m ? 1 : 0;
+    }
+    const int sl = cslot[u];
+    uk[r] = unmap_key(m);
+    if (sl >= 0) {
+      fi[r] = hmin[sl];
+      if (cnt) cnt[r] = hcnt[sl];
+      hmin[sl] = r;   // (this thread is the only one that reads the slot here)
+    } else {
+      fi[r] = zmin;
+      if (cnt) cnt[r] = zcnt;
+      zgroup = r;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < kHashPer; ++e) {
+    const int p = tid + e * kSmallThreads;
+    if (p < R) inv[p] = myslot[e] >= 0 ? hmin[myslot[e]] : zgroup;
+  }
+  if (tid == 0) *nu_out = (int64_t)n;
 }
 
 // ---------------------------------------------------------------- radix path
@@ -401,6 +513,11 @@ size_t dedup_workspace_bytes(int64_t R) {
 
 hipError_t launch_dedup(const int64_t *keys, int64_t R, int64_t *uk, int32_t *fi, int32_t *cnt,
                         int32_t *inv, int64_t *nu, void *ws, hipStream_t st) {
+  if (R <= kHashMax) {
+    hipLaunchKernelGGL(dedup_hash_kernel, dim3(1), dim3(kSmallThreads), 0, st, keys, (int)R, uk,
+                       fi, cnt, inv, nu);
+    return hipGetLastError();
+  }
   if (R <= kSmallMax) {
     int P = 1;
     while (P < R) P <<= 1;

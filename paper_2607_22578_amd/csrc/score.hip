@@ -228,18 +228,23 @@ __global__ __launch_bounds__(kThreads) void score_partial_valu(ScoreArgs a) {
 // ---------------------------------------------------------------- merge
 
 constexpr int kMergeThreads = 1024;
+constexpr int kMergeRankMax = 2048;   // survivors ranked by counting up to this many
 
 // One workgroup per distinct query.  Its S*k slice keys are compacted into
-// LDS, dropping empty keys and, when a shared threshold is given, keys whose
-// score is below it (a lower bound of the query's k-th best score, so every
-// key of the final k survives); the survivors are sorted (bitonic,
-// descending) and the first k decoded to (score, row), ranks past the
-// survivors padded with (-inf, -1).
+// LDS, dropping empty keys, keys below the k-th largest list head when the
+// lists are sorted, and, when a shared threshold is given, keys whose score
+// is below it (each a lower bound of the query's k-th best, so every key of
+// the final k survives); the survivors are sorted (bitonic,
+// descending; up to kMergeRankMax survivors are ranked by counting the
+// survivors above each instead) and the first k decoded to (score, row),
+// ranks past the survivors padded with (-inf, -1).
 __global__ __launch_bounds__(kMergeThreads) void topk_merge_kernel(
     const uint64_t *__restrict__ part, const uint32_t *__restrict__ thr, int64_t n_unique,
     const int64_t *__restrict__ n_unique_dev, int64_t cap, int64_t N, int k, int mq, int nc,
-    int64_t smax, int grid, float *__restrict__ out_s, int32_t *__restrict__ out_i) {
-  __shared__ uint64_t buf[kMaxSK];
+    int64_t smax, int grid, int sorted, float *__restrict__ out_s, int32_t *__restrict__ out_i) {
+  __shared__ uint64_t buf[kMaxSK + 8];
+  __shared__ uint64_t heads[kMergeThreads];
+  __shared__ uint64_t head_cut;
   __shared__ int count;
   const int64_t nu = read_nu(n_unique, n_unique_dev, cap);
   const Split sp = make_split(nu, N, mq, nc, grid, smax);
@@ -248,12 +253,29 @@ __global__ __launch_bounds__(kMergeThreads) void topk_merge_kernel(
   for (int64_t q = blockIdx.x; q < nu; q += gridDim.x) {
     const uint32_t t = thr ? thr[q] : 0u;
     const uint64_t *src = part + q * sp.S * k;
-    if (tid == 0) count = 0;
+    if (tid == 0) {
+      count = 0;
+      head_cut = 0ull;
+    }
+    // With lists sorted in descending order, the k-th largest of the S list
+    // heads is also a lower bound of the query's k-th best key: the heads
+    // are keys of distinct rows (empty heads are 0 and tie, leaving the cut
+    // at 0 when fewer than k slices kept anything).
+    const bool use_heads = sorted && sp.S >= k && sp.S <= kMergeThreads;
+    if (use_heads && tid < sp.S) heads[tid] = src[(int64_t)tid * k];
     __syncthreads();
+    if (use_heads && tid < sp.S) {
+      const uint64_t hk = heads[tid];
+      int r = 0;
+      for (int j = 0; j < (int)sp.S; ++j) r += heads[j] > hk ? 1 : 0;
+      if (r == k - 1 && hk != 0ull) head_cut = hk;
+    }
+    __syncthreads();
+    const uint64_t cut = head_cut;
     for (int i0 = 0; i0 < n; i0 += kMergeThreads) {
       const int i = i0 + tid;
       const uint64_t key = i < n ? src[i] : 0ull;
-      const bool keep = key != 0ull && (uint32_t)(key >> 32) >= t;
+      const bool keep = key != 0ull && (uint32_t)(key >> 32) >= t && key >= cut;
       const uint64_t mask = __builtin_amdgcn_ballot_w64(keep);
       int base = 0;
       if (lane == 0 && mask) base = atomicAdd(&count, __popcll(mask));
@@ -262,31 +284,62 @@ __global__ __launch_bounds__(kMergeThreads) void topk_merge_kernel(
     }
     __syncthreads();
     const int m = count;
-    int P = 2;
-    while (P < m) P <<= 1;
-    for (int i = m + tid; i < P; i += kMergeThreads) buf[i] = 0ull;
-    __syncthreads();
-    for (int size = 2; size <= P; size <<= 1) {
-      for (int stride = size >> 1; stride > 0; stride >>= 1) {
-        for (int u = tid; u < (P >> 1); u += kMergeThreads) {
-          const int i = 2 * u - (u & (stride - 1));
-          const int j = i + stride;
-          const bool desc = (i & size) == 0;
-          const uint64_t x = buf[i], y = buf[j];
-          if ((x < y) == desc) {
-            buf[i] = y;
-            buf[j] = x;
-          }
+    if (m <= kMergeRankMax) {
+      // rank = number of survivors above (keys are distinct: one per row);
+      // the survivors are padded with empty keys to a multiple of 8 so that
+      // eight independent reads are in flight at a time
+      const int m8 = (m + 7) & ~7;
+      for (int i = m + tid; i < m8; i += kMergeThreads) buf[i] = 0ull;
+      __syncthreads();
+      for (int u = tid; u < m; u += kMergeThreads) {
+        const uint64_t key = buf[u];
+        int r = 0;
+        for (int j = 0; j < m8; j += 8) {
+          uint64_t b[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) b[t] = buf[j + t];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) r += b[t] > key ? 1 : 0;
         }
-        __syncthreads();
+        if (r < k) {
+          float sc;
+          int32_t row;
+          decode_key(key, sc, row);
+          out_s[q * k + r] = sc;
+          out_i[q * k + r] = row;
+        }
       }
-    }
-    for (int j = tid; j < k; j += kMergeThreads) {
-      float sc;
-      int32_t row;
-      decode_key(j < m ? buf[j] : 0ull, sc, row);
-      out_s[q * k + j] = sc;
-      out_i[q * k + j] = row;
+      for (int j = m + tid; j < k; j += kMergeThreads) {
+        out_s[q * k + j] = -__builtin_inff();
+        out_i[q * k + j] = -1;
+      }
+    } else {
+      int P = 2;
+      while (P < m) P <<= 1;
+      for (int i = m + tid; i < P; i += kMergeThreads) buf[i] = 0ull;
+      __syncthreads();
+      for (int size = 2; size <= P; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+          for (int u = tid; u < (P >> 1); u += kMergeThreads) {
+            const int i = 2 * u - (u & (stride - 1));
+            const int j = i + stride;
+            const bool desc = (i & size) == 0;
+            const uint64_t x = buf[i], y = buf[j];
+            if ((x < y) == desc) {
+              buf[i] = y;
+              buf[j] = x;
+            }
+          }
+          __syncthreads();
+        }
+      }
+      for (int j = tid; j < k; j += kMergeThreads) {
+        float sc;
+        int32_t row;
+        decode_key(j < m ? buf[j] : 0ull, sc, row);
+        out_s[q * k + j] = sc;
+        out_i[q * k + j] = row;
+      }
     }
     __syncthreads();
   }
@@ -400,7 +453,7 @@ hipError_t launch_topk_merge(const void *part, int64_t n_unique, const int64_t *
   if (blocks > 2 * (int64_t)grid) blocks = 2 * (int64_t)grid;
   hipLaunchKernelGGL(topk_merge_kernel, dim3((unsigned)blocks), dim3(kMergeThreads), 0, st,
                      (const uint64_t *)part, thr, n_unique, nu_dev, cap, N, k, mq, nc, smax, grid,
-                     out_s, out_i);
+                     valu ? 0 : 1, out_s, out_i);
   return hipGetLastError();
 }
 

@@ -1,4 +1,6 @@
 """Dedup on the GPU, bit-exact against the oracle."""
+import zlib
+
 import numpy as np
 import pytest
 import torch
@@ -52,9 +54,11 @@ def test_dedup_workload_keys(name):
                                   "distinct_small", "distinct_radix", "extremes_small",
                                   "extremes_radix", "negative", "boundary_4096",
                                   "boundary_4097", "ragged_radix", "narrow_range_radix",
-                                  "wide_and_narrow"])
+                                  "wide_and_narrow", "all_min_hash", "distinct_hash",
+                                  "boundary_2048", "boundary_2049", "high_bits_hash"])
 def test_dedup_edge_cases(case):
-    rng = np.random.default_rng(abs(hash(case)) % (2 ** 32))
+    # paths: hash table up to 2,048 keys, bitonic sort up to 4,096, radix sort
+    rng = np.random.default_rng(zlib.crc32(case.encode()))
     if case == "one":
         keys = np.array([12345], np.int64)
     elif case == "two_equal":
@@ -78,6 +82,16 @@ def test_dedup_edge_cases(case):
         keys = rng.integers(0, 1000, size=4096).astype(np.int64)
     elif case == "boundary_4097":
         keys = rng.integers(0, 1000, size=4097).astype(np.int64)
+    elif case == "all_min_hash":              # only the key that maps to 0
+        keys = np.full(2048, I64_MIN, np.int64)
+    elif case == "distinct_hash":
+        keys = rng.integers(I64_MIN, I64_MAX, size=2048, dtype=np.int64, endpoint=True)
+    elif case == "boundary_2048":
+        keys = rng.integers(-50, 50, size=2048).astype(np.int64)
+    elif case == "boundary_2049":
+        keys = rng.integers(-50, 50, size=2049).astype(np.int64)
+    elif case == "high_bits_hash":            # keys that differ only in their top bits
+        keys = (rng.integers(0, 4096, size=1500).astype(np.int64) << 52)
     elif case == "ragged_radix":
         keys = rng.integers(-2 ** 40, 2 ** 40, size=3 * 4096 + 77).astype(np.int64)
     elif case == "narrow_range_radix":        # 18-bit span, far from zero
