@@ -989,13 +989,11 @@ static hipError_t launch_mfma(K kern, int grid, int lds, const MfmaArgs &a, hipS
   return hipGetLastError();
 }
 
-__global__ void mfma_gthr_init(uint32_t *g, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) g[i] = 0u;
-}
-
 // Threshold seed per distinct query: the k-th largest of its lane maxima
-// from the seed pass (at most kSeedMax of them), written to gthr.  Radix
+// from the seed pass (at most kSeedMax of them), written to gthr, which it
+// thereby (re)starts for the call: 0, no threshold, where there is no seed.
+// The seed pass reads gthr only with its copies and never uses the values.
+// Radix
 // select on the 32-bit ordered scores, 8 bits per pass: a pass counts the
 // values that carry the digits chosen so far by their next digit, and keeps
 // the largest digit whose count of values at or above it reaches the rank
@@ -1012,8 +1010,13 @@ __global__ __launch_bounds__(kSeedThreads) void mfma_seed_kernel(
   const Split sp = make_split(nu, N, kMMQ, kMNC, grid, smax);
   const int64_t per = sp.S * kMLanesQ;
   const int n = (int)(per < kSeedMax ? per : kSeedMax);
-  if (n < k) return;   // fewer lane maxima than k: no seed
   const int tid = threadIdx.x;
+  if (n < k) {   // fewer lane maxima than k: no seed
+    for (int64_t q = (int64_t)blockIdx.x * kSeedThreads + tid; q < nu;
+         q += (int64_t)gridDim.x * kSeedThreads)
+      gthr[q] = 0u;
+    return;
+  }
   for (int64_t q = blockIdx.x; q < nu; q += gridDim.x) {
     const uint32_t *src = lmax + q * per;
     for (int i = tid; i < n; i += kSeedThreads) vals[i] = src[i];
@@ -1062,7 +1065,7 @@ __global__ __launch_bounds__(kSeedThreads) void mfma_seed_kernel(
       // (hist was last read before the barrier above; sel is rewritten only
       // after the next pass's counting barrier)
     }
-    if (tid == 0 && prefix) gthr[q] = prefix;
+    if (tid == 0) gthr[q] = prefix;
     __syncthreads();
   }
 }
@@ -1070,17 +1073,10 @@ __global__ __launch_bounds__(kSeedThreads) void mfma_seed_kernel(
 hipError_t launch_score_mfma(const void *q, const void *corpus, const float *scale, int64_t N,
                              int64_t d, int k, int64_t n_unique, const int64_t *nu_dev,
                              int64_t cap, bool fp8, void *ws, hipStream_t st) {
-  // shared thresholds start empty on every call (a fill kernel, so that the
-  // sequence can be captured in a graph)
+  // shared thresholds: (re)started by the seed selection on every call
   uint32_t *gthr = (uint32_t *)ws;
   uint32_t *lmax = (uint32_t *)((unsigned char *)ws + mfma_thr_bytes(cap));
   void *part = (unsigned char *)ws + mfma_part_offset(cap, N, k, kMGridMax);
-  if (cap > 0) {
-    hipLaunchKernelGGL(mfma_gthr_init, dim3((unsigned)((cap + 255) / 256)), dim3(256), 0, st,
-                       gthr, cap);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
   MfmaArgs a;
   a.q = q;
   a.corpus = corpus;
