@@ -315,7 +315,7 @@ struct MLds {
   float *thr0;       // [MQ] warm-up threshold of the item
   float *thr;        // [MQ] current threshold
   uint32_t *pub;     // [MQ] last threshold published to the shared array
-  uint64_t *lmin;    // [MQ] last (smallest) key of the sorted list, 0 while not full
+  uint64_t *lmin;    // [MQ] last key of the sorted list when full, else its fill count
   float *warm;       // [kMW][MQ] per-wave minima of group maxima (aliases queue)
   int32_t *flags;    // [1] overflow epoch, [2] half-full epoch
   uint64_t *lists;   // [MQ][k] or nullptr (lists in the global partial buffer)
@@ -382,58 +382,40 @@ __device__ __forceinline__ void merge_queue(const MLds &L, const MfmaArgs &a, co
   if (cnt <= 0) return;
   const int n = cnt < kMQcap ? cnt : kMQcap;
   const int k = a.k;
+  const int hb = LDS_LISTS ? k : k - kMTail;   // first position held in the LDS tail
+  uint64_t *l = LDS_LISTS ? L.lists + t * k
+                          : a.part + ((int64_t)(it.qbase + t) * it.S + it.s) * k;
+  uint64_t *tail = LDS_LISTS ? nullptr : L.tail + t * kMTail;
+  auto get = [&](int i) -> uint64_t { return (!LDS_LISTS && i >= hb) ? tail[i - hb] : l[i]; };
+  auto set = [&](int i, uint64_t v) {
+    if (!LDS_LISTS && i >= hb)
+      tail[i - hb] = v;
+    else
+      l[i] = v;
+  };
+  // lmin holds the list's last key once the list is full, else its fill
+  // count (below 2^32, hence below every key: a real key's ordered score is
+  // nonzero), so that an entrant of a list that is not full starts at the
+  // first empty slot instead of climbing over the empty ones
   uint64_t mn = L.lmin[t];
-  if constexpr (LDS_LISTS) {
-    uint64_t *l = L.lists + t * k;
-    for (int e = 0; e < n; ++e) {
-      const uint64_t key = L.queue[t * kMQcap + e];
-      if (key > mn) {
-        int i = k - 1;
-        while (i > 0) {
-          const uint64_t prev = l[i - 1];
-          if (prev > key) break;
-          l[i] = prev;
-          --i;
-        }
-        l[i] = key;
-        mn = l[k - 1];
+  int fill = (mn >> 32) ? k : (int)mn;
+  for (int e = 0; e < n; ++e) {
+    const uint64_t key = L.queue[t * kMQcap + e];
+    if (key > mn) {
+      int i = fill < k ? fill : k - 1;
+      while (i > 0) {
+        const uint64_t prev = get(i - 1);
+        if (prev > key) break;
+        set(i, prev);
+        --i;
       }
-    }
-  } else {
-    const int hb = k - kMTail;   // first position held in LDS
-    uint64_t *head = a.part + ((int64_t)(it.qbase + t) * it.S + it.s) * k;
-    uint64_t *tl = L.tail + t * kMTail;
-    for (int e = 0; e < n; ++e) {
-      const uint64_t key = L.queue[t * kMQcap + e];
-      if (key > mn) {
-        int i = k - 1;
-        while (i > hb) {
-          const uint64_t prev = tl[i - 1 - hb];
-          if (prev > key) break;
-          tl[i - hb] = prev;
-          --i;
-        }
-        if (i == hb) {
-          while (i > 0) {
-            const uint64_t prev = head[i - 1];
-            if (prev > key) break;
-            if (i == hb)
-              tl[0] = prev;
-            else
-              head[i] = prev;
-            --i;
-          }
-        }
-        if (i >= hb)
-          tl[i - hb] = key;
-        else
-          head[i] = key;
-        mn = tl[kMTail - 1];
-      }
+      set(i, key);
+      if (fill < k) ++fill;
+      mn = fill == k ? get(k - 1) : (uint64_t)fill;
     }
   }
   L.lmin[t] = mn;
-  const float tl = mn ? unord_score((uint32_t)(mn >> 32)) : -__builtin_inff();
+  const float tl = (mn >> 32) ? unord_score((uint32_t)(mn >> 32)) : -__builtin_inff();
   const float t0v = L.thr0[t];
   L.thr[t] = tl > t0v ? tl : t0v;
   publish_thr(L, a, it, t, L.thr[t]);
