@@ -402,12 +402,35 @@ __device__ __forceinline__ void merge_queue(const MLds &L, const MfmaArgs &a, co
   for (int e = 0; e < n; ++e) {
     const uint64_t key = L.queue[t * kMQcap + e];
     if (key > mn) {
-      int i = fill < k ? fill : k - 1;
-      while (i > 0) {
-        const uint64_t prev = get(i - 1);
-        if (prev > key) break;
-        set(i, prev);
-        --i;
+      int i = fill < k ? fill : k - 1;   // the key's slot if no entry above is smaller
+      if constexpr (LDS_LISTS) {
+        while (i > 0) {
+          const uint64_t prev = get(i - 1);
+          if (prev > key) break;
+          set(i, prev);
+          --i;
+        }
+      } else {
+        // climb in windows of 8 entries read together (independent global
+        // loads): the window's entries above the key stay, the others move
+        // down by one
+        while (i > 0) {
+          const int lo = i > 8 ? i - 8 : 0;
+          uint64_t b[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) b[u] = lo + u < i ? get(lo + u) : 0ull;   // (0: not above)
+          int above = 0;
+#pragma unroll
+          for (int u = 0; u < 8; ++u) above += b[u] > key ? 1 : 0;
+#pragma unroll
+          for (int u = 7; u >= 0; --u)
+            if (u >= above && lo + u < i) set(lo + u + 1, b[u]);
+          if (above > 0 || lo == 0) {
+            i = lo + above;
+            break;
+          }
+          i = lo;
+        }
       }
       set(i, key);
       if (fill < k) ++fill;
