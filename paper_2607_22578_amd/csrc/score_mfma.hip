@@ -501,6 +501,44 @@ __device__ __forceinline__ void finish_scores(f32x16m (&acc)[kMRB][kMQB], const 
     pin_acc(acc);
   }
 }
+// NaN for the scores of rows past N (only for a tile that reaches past N).
+__device__ __forceinline__ void mask_tail(f32x16m (&acc)[kMRB][kMQB], int lim0) {
+  if (lim0 < 32 * kMRB) {   // some of this lane's rows are past N
+    const float nan = __builtin_nanf("");
+#pragma unroll
+    for (int rb = 0; rb < kMRB; ++rb)
+#pragma unroll
+      for (int qb = 0; qb < kMQB; ++qb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (rb * 32 + 8 * (i >> 2) + (i & 3) >= lim0) acc[rb][qb][i] = nan;
+    pin_acc(acc);
+  }
+}
+
+// The 16 fp8 row scales of row block rb of this lane (rows rb * 32 + 8 * (i /
+// 4) + i % 4 from the lane's first row), or ones when the accumulators are
+// already scaled.
+template <bool FP8>
+__device__ __forceinline__ void row_scales(float (&s16)[16], const float *ssc_lane, int rb,
+                                           bool ones) {
+  if constexpr (FP8) {
+    if (!ones) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float4 s4 = *reinterpret_cast<const float4 *>(ssc_lane + rb * 32 + 8 * j);
+        s16[4 * j + 0] = s4.x;
+        s16[4 * j + 1] = s4.y;
+        s16[4 * j + 2] = s4.z;
+        s16[4 * j + 3] = s4.w;
+      }
+      return;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) s16[i] = 1.0f;
+}
+
 
 // Warm-up: per query, the smallest of this lane's group maxima (groups of
 // SPAN consecutive scores), combined over the two lane halves and stored per
@@ -571,8 +609,15 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
   const int lim0 = (int)a.N - row0 - lrow;
   const float *ssc_lane = FP8 ? ssc + lrow : nullptr;
   pin_acc(acc);
-  finish_scores<FP8>(acc, ssc_lane, lim0);
+  // fp8: scores are accumulator x row scale.  Only an item's first tile
+  // (warm-up) scales the accumulators in place; otherwise the screening and
+  // the examined blocks multiply as they read.
   const int gpl = mwarm_groups(a.k);
+  const bool scaled = FP8 && first && gpl > 0;
+  if (scaled)
+    finish_scores<FP8>(acc, ssc_lane, lim0);
+  else
+    mask_tail(acc, lim0);
   if (first && gpl > 0) {
     // warm-up threshold: the smallest of kMLanesQ * gpl group maxima (the
     // queue, which these minima alias, is empty at an item's first tile)
@@ -615,18 +660,22 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
   pin_acc(acc);
   uint64_t elig[kMQB];
 #pragma unroll
-  for (int qb = 0; qb < kMQB; ++qb) {
-    const float th = thr_r[qb];
-    uint64_t e = 0;
+  for (int qb = 0; qb < kMQB; ++qb) elig[qb] = 0ull;
 #pragma unroll
-    for (int rb = 0; rb < kMRB; ++rb) {
+  for (int rb = 0; rb < kMRB; ++rb) {
+    float s16[16];
+    row_scales<FP8>(s16, ssc_lane, rb, scaled);
+#pragma unroll
+    for (int qb = 0; qb < kMQB; ++qb) {
       float m = ninf;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) m = fmaxf(m, acc[rb][qb][i]);
-      e |= m >= th ? 0xFFFFull << (16 * rb) : 0ull;
+      for (int i = 0; i < 16; ++i) m = fmaxf(m, FP8 ? acc[rb][qb][i] * s16[i] : acc[rb][qb][i]);
+      elig[qb] |= m >= thr_r[qb] ? 0xFFFFull << (16 * rb) : 0ull;
     }
-    elig[qb] = qb * 32 + c < it.qvalid ? e : 0ull;
   }
+#pragma unroll
+  for (int qb = 0; qb < kMQB; ++qb)
+    if (qb * 32 + c >= it.qvalid) elig[qb] = 0ull;
   // Scores at or above the current threshold are appended to the per-query
   // LDS queues (atomics, no barrier).  Merges into the k-lists are deferred:
   // one barrier per tile checks whether some queue overflowed (its
@@ -645,11 +694,12 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
       for (int rb = 0; rb < kMRB; ++rb) {
         const uint32_t el = (uint32_t)(elig[qb] >> (16 * rb)) & 0xFFFFu;
         if (!__builtin_amdgcn_ballot_w64(el != 0)) continue;
-        float v[16];
+        float v[16], s16[16];
+        row_scales<FP8>(s16, ssc_lane, rb, scaled);
         uint32_t cand = 0;
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          v[i] = acc[rb][qb][i];
+          v[i] = FP8 ? acc[rb][qb][i] * s16[i] : acc[rb][qb][i];
           cand |= v[i] >= th ? 1u << i : 0u;
         }
         cand &= el;
