@@ -2,7 +2,8 @@
 the oracle (acceptance rule of oracle/accept.py): dimensions that leave a
 partial last K stage (the copies read zeros past d), corpora smaller than
 one 384-row tile or with a ragged last tile, k-lists held in global memory
-instead of LDS, and k too large for the first-pass threshold seed."""
+instead of LDS, k too large for the first-pass threshold seed, and a merge
+with more survivors than it ranks by counting (it sorts them)."""
 import numpy as np
 import pytest
 
@@ -62,4 +63,18 @@ def test_k_beyond_seed():
     m = run_merge(w.keys, q, c, k)
     ref = check_dedup(m, w.keys)
     check_unique_topk(m, ref, q, c, k)
+    check_delivery(m, w.R)
+
+
+def test_large_k_many_survivors():
+    # k = 300 over 200,000 rows: fewer slices than k (no head cut), fewer lane
+    # maxima than k (no seed) and no warm-up, so the cross-slice merge keeps
+    # most of the 27 x 300 list keys and sorts them instead of ranking
+    w, q, c, _ = _stream(200_000, 64, "bf16")
+    k = 300
+    note(f"bf16 k={k} N=200000 d=64")
+    m = run_merge(w.keys, q, c, k)
+    ref = check_dedup(m, w.keys)
+    sel = np.random.default_rng(7).choice(ref["n_unique"], size=48, replace=False)
+    check_unique_topk(m, ref, q, c, k, sel=np.sort(sel))
     check_delivery(m, w.R)
