@@ -31,25 +31,29 @@
 // both operands agree; each lane takes the K slice that makes its fp8 corpus
 // piece one 16-byte read.
 //
-// Synchronisation per stage: after three of its four MFMA steps the waves
-// wait for their own copies of the next stage (s_waitcnt vmcnt with the exact
-// number of younger copies), then one barrier, then the next copies and the
-// next stage's first fragments, overlapped with the last step.  The fences
-// of __syncthreads are not used because they would wait for every copy in
-// flight.
+// Synchronisation per stage: a wave copies, and alone reads, its own 96
+// corpus rows of a stage, so it refills them as soon as its own reads of
+// the stage's slot are complete (after the first of the four MFMA steps),
+// without a barrier.  The query rows are shared by the four waves: after the
+// third step the waves wait for their own copies of the next stage
+// (s_waitcnt vmcnt with the number of younger copies), then one barrier,
+// then the query rows of the stage ns ahead and the next stage's first
+// fragments, overlapped with the last step.  The fences of __syncthreads are
+// not used because they would wait for every copy in flight.
 //
-// Top-k (fused, scores never reach memory), per tile: fp8 row scales
-// multiply the scores, rows past N are masked, and each lane compares the
-// maxima of its half blocks (8 scores) with the query's threshold; only
-// scores at or above it are appended to a small per-query LDS queue, merged
-// into the query's sorted k-list when a queue fills.  Thresholds come from
-// three lower bounds of the query's final k-th best score: the slice's own
-// k-list; a seed, the k-th largest of the lane maxima of a first pass over
-// one tile of every slice (a sample spread over the corpus); and the largest
-// bound any slice of the query has published so far (a per-query array in
-// the workspace, read asynchronously with each tile's copies).  Keys order
-// by (score desc, row asc): ties go to the lower corpus row independently of
-// tile, slice or lane.
+// Top-k (fused, scores never reach memory), per tile: rows past N are
+// masked and each lane screens its 16-score row blocks by their maximum
+// (fp8: accumulator x row scale) against the query's threshold; only the
+// blocks that reach it are examined, and their scores at or above it are
+// appended to a small per-query LDS queue (one atomic per lane and block
+// reserves the slots), merged into the query's sorted k-list when a queue
+// fills.  Thresholds come from three lower bounds of the query's final k-th
+// best score: the slice's own k-list; a seed, the k-th largest of the lane
+// maxima of a first pass over one tile of every slice (a sample spread over
+// the corpus); and the largest bound any slice of the query has published so
+// far (a per-query array in the workspace, read asynchronously with each
+// tile's copies).  Keys order by (score desc, row asc): ties go to the lower
+// corpus row independently of tile, slice or lane.
 #include <type_traits>
 
 #include "common.h"
