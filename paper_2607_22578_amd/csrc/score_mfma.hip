@@ -63,7 +63,6 @@ namespace hs {
 typedef __bf16 bf16x8m __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2m __attribute__((ext_vector_type(2)));
 typedef float f32x16m __attribute__((ext_vector_type(16)));
-typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kMW = 4;                   // waves per workgroup (one per SIMD)
 constexpr int kMT = kMW * 64;            // threads
@@ -346,11 +345,6 @@ __device__ __forceinline__ MLds carve_mlds(unsigned char *p, int k) {
   L.tail = LDS_LISTS ? nullptr : reinterpret_cast<uint64_t *>(p);
   (void)k;
   return L;
-}
-
-// Row of accumulator element i of 32-row block rb, relative to the tile.
-__device__ __forceinline__ int macc_row(int wv, int rb, int h, int i) {
-  return wv * 32 * kMRB + rb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
 }
 
 struct MItem {
