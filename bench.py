@@ -66,8 +66,12 @@ def parse():
     ap.add_argument("--workload", default="ridge1m",
                     help="ridge1m (default), mfma4m or fp8_20m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=int, default=48,
+    ap.add_argument("--cpu-sample", type=int, default=96,
                     help="distinct queries scored by the oracle for the CPU baseline")
+    ap.add_argument("--no-merge", action="store_true",
+                    help="ablation: every request is scored on its own (no dedup merge)")
+    ap.add_argument("--corpus-rows", type=int, default=0,
+                    help="override the corpus size (e.g. one GPU's shard of a sharded corpus)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
     return ap.parse_args()
@@ -103,8 +107,11 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     t_gen = time.time()
-    w = synth.make(args.workload)
+    w = synth.make(args.workload, n_corpus=args.corpus_rows or None)
     t_gen = time.time() - t_gen
+    if args.no_merge:
+        # every request its own key: the same rows and corpus, scored unmerged
+        w.keys = np.arange(w.R, dtype=np.int64)
     cfg = w.cfg
     R, d, N, k = w.R, w.dim, w.n_corpus, w.k
     qdt = hs.HS_BF16
@@ -154,7 +161,8 @@ def main():
     wall = time.perf_counter() - wall0
     total_ms = t_start.elapsed_time(t_end)
     ms_per_step = total_ms / args.steps
-    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in evs.values()]))
+    kern_samples = np.array([a.elapsed_time(b) for a, b in evs.values()])
+    kern_ms = float(np.mean(kern_samples))
 
     # stage breakdown (separate, untimed-for-value pass)
     st_ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
@@ -196,6 +204,8 @@ def main():
     roof["traffic"] = None
     roof["kernel"] = SCORE_STEP
     roof["kernel_ms"] = round(kern_ms, 4)
+    roof["kernel_ms_p10_p50_p90"] = [round(float(np.percentile(kern_samples, p)), 4)
+                                     for p in (10, 50, 90)]
     roof["algorithmic_bytes"] = alg_bytes
     roof["algorithmic_flops"] = alg_flops
     roof["hbm_gbs_algorithmic"] = round(gbs, 1)
@@ -216,7 +226,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {cfg.desc}", "n_requests": R, "n_unique": n_u,
                    "dim": d, "n_corpus": N, "k": k, "query_dtype": cfg.q_enc,
-                   "corpus_dtype": cfg.c_enc, "seed": w.seed},
+                   "corpus_dtype": cfg.c_enc, "seed": w.seed,
+                   "merge": not args.no_merge},
         "unique_queries_per_s": round(n_u * args.steps / (total_ms * 1e-3), 1),
         "stages_ms": stages,
         "wall_s_timed": round(wall, 4),
@@ -247,8 +258,14 @@ def cpu_baseline(w, n_u: int, n_sample: int) -> dict:
     oracle.topk_exact(rows, w.corpus, w.k, scale=w.scale, q_rows=sel, threads=threads)
     t_score = time.perf_counter() - t1
     t_full = t_dedup + t_score * ref["n_unique"] / n_sample
+    cpu = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
+    except OSError:
+        pass
     return {"value": round(w.R / t_full, 2), "unit": "queries/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu,
             "sample": f"dedup+gather of all {w.R} requests, exact fp64 top-{w.k} of "
                       f"{n_sample}/{ref['n_unique']} distinct queries over all {w.n_corpus} "
                       f"rows ({t_score:.1f} s), extrapolated to all distinct queries",
