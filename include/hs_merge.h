@@ -21,6 +21,8 @@
  *                  the corpus (retrieval with Top-K among its parameters,
  *                  Eq. 2; top-K vector retrieval of the RAG workloads, Sec. 4.1)
  *                  = hs_score_partial followed by hs_topk_merge.
+ * Optionally, hs_cache_lookup / hs_cache_insert reuse results across windows
+ * (Sec. 3.3 (II)), so that only keys not seen before are scored.
  *
  * Conventions (all entry points):
  *   - Every function returns hs_status.  Arguments are validated on the host
@@ -161,6 +163,58 @@ hs_status hs_topk_merge(const hs_plan *plan, int64_t n_unique, const int64_t *n_
 hs_status hs_scatter(const void *src, int64_t src_rows, int64_t row_bytes,
                      const void *index, int32_t index_is_i64, int64_t n_out,
                      const int64_t *n_out_dev, void *dst, void *stream);
+
+/* Cross-window reuse (Sec. 3.3 (II), asynchronous cache reuse): a node whose
+ * signature matches a node completed in an earlier window takes that node's
+ * result instead of being executed again.  The store lives in one caller-owned
+ * device buffer and holds at most `capacity` top-k rows of the plan's k:
+ *   layout   keys [C] int64 | valid [C] int32 | claim [C] int32 |
+ *            score [C x k] fp32 | index [C x k] int32, each array starting on a
+ *            256-byte boundary (C = capacity, a power of two in [1, 2^30]);
+ *   mapping  direct-mapped, slot(key) = top log2(C) bits of
+ *            key * 0x9E3779B97F4A7C15 (mod 2^64), one entry per slot; a hit
+ *            needs a valid slot holding the same key;
+ *   insert   the misses of a window are stored; where several map to one
+ *            slot, the largest key wins; an insert replaces the slot's entry.
+ * The content after every window depends only on the windows' keys and
+ * results, never on thread timing.  Stored rows are those of the corpus the
+ * window was scored against: call hs_cache_reset when the corpus changes.
+ * Calls on one store must not overlap (same stream, or ordered by events). */
+
+/* *bytes = size of the store buffer for `capacity` entries of the plan's k. */
+hs_status hs_cache_bytes(const hs_plan *plan, int64_t capacity, size_t *bytes);
+
+/* Empties the store (every slot invalid).  Needed once before first use. */
+hs_status hs_cache_reset(const hs_plan *plan, void *cache, size_t cache_bytes, int64_t capacity,
+                         void *stream);
+
+/* Looks up the window's distinct keys (hs_dedup's unique_keys / first_index,
+ * with n_unique / n_unique_dev as for hs_score_topk):
+ *   topk_score/index [n_u x k] out: rows of the hits are filled with the
+ *                    stored result; rows of the misses are left untouched
+ *   miss_pos   [n_u] int32 out: -1 for a hit, else the miss's position in
+ *              the miss list (misses numbered in ascending key order)
+ *   miss_first [n_u] int32 out: entry p (< n_miss) = first_index of miss p,
+ *              i.e. the request whose query row represents it (entries from
+ *              n_miss on are unspecified)
+ *   n_miss_dev int64 device out: number of misses n_m
+ * The misses are then scored as a window of n_m distinct nodes (query rows
+ * gathered through miss_first, hs_score_topk with n_unique_dev = n_miss_dev)
+ * and their rows put back in place with hs_scatter(index = miss_pos), which
+ * leaves the hit rows alone. */
+hs_status hs_cache_lookup(const hs_plan *plan, void *cache, size_t cache_bytes, int64_t capacity,
+                          const int64_t *unique_keys, const int32_t *first_index,
+                          int64_t n_unique, const int64_t *n_unique_dev, float *topk_score,
+                          int32_t *topk_index, int32_t *miss_pos, int32_t *miss_first,
+                          int64_t *n_miss_dev, void *stream);
+
+/* Stores the rows of the window's misses (miss_pos from hs_cache_lookup on
+ * the same store, no other call on it in between; topk_score/index are the
+ * window's complete [n_u x k] rows). */
+hs_status hs_cache_insert(const hs_plan *plan, void *cache, size_t cache_bytes, int64_t capacity,
+                          const int64_t *unique_keys, const int32_t *miss_pos, int64_t n_unique,
+                          const int64_t *n_unique_dev, const float *topk_score,
+                          const int32_t *topk_index, void *stream);
 
 const char *hs_status_string(hs_status s);
 const char *hs_last_error(void);

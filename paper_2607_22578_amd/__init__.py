@@ -36,7 +36,8 @@ HS_F32, HS_BF16, HS_FP8_E4M3 = 0, 1, 2
 ABI_VERSION = 1
 
 EXPORTS = ["hs_merge_plan", "hs_plan_destroy", "hs_dedup", "hs_score_topk", "hs_score_partial",
-           "hs_topk_merge", "hs_scatter", "hs_status_string", "hs_last_error", "hs_abi_version"]
+           "hs_topk_merge", "hs_scatter", "hs_cache_bytes", "hs_cache_reset", "hs_cache_lookup",
+           "hs_cache_insert", "hs_status_string", "hs_last_error", "hs_abi_version"]
 
 
 class hs_merge_desc(ctypes.Structure):
@@ -62,6 +63,14 @@ _lib.hs_topk_merge.argtypes = [_vp, _i64, _vp, _vp, _vp, _vp, _sz, _vp]
 _lib.hs_topk_merge.restype = ctypes.c_int
 _lib.hs_scatter.argtypes = [_vp, _i64, _i64, _vp, _i32, _i64, _vp, _vp, _vp]
 _lib.hs_scatter.restype = ctypes.c_int
+_lib.hs_cache_bytes.argtypes = [_vp, _i64, ctypes.POINTER(_sz)]
+_lib.hs_cache_bytes.restype = ctypes.c_int
+_lib.hs_cache_reset.argtypes = [_vp, _vp, _sz, _i64, _vp]
+_lib.hs_cache_reset.restype = ctypes.c_int
+_lib.hs_cache_lookup.argtypes = [_vp, _vp, _sz, _i64, _vp, _vp, _i64] + [_vp] * 7
+_lib.hs_cache_lookup.restype = ctypes.c_int
+_lib.hs_cache_insert.argtypes = [_vp, _vp, _sz, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp]
+_lib.hs_cache_insert.restype = ctypes.c_int
 _lib.hs_status_string.argtypes = [ctypes.c_int]
 _lib.hs_status_string.restype = ctypes.c_char_p
 _lib.hs_last_error.argtypes = []
@@ -190,6 +199,36 @@ def hs_scatter(src, src_rows: int, row_bytes: int, index, index_is_i64: int, n_o
                            _ptr(n_out_dev), _ptr(dst), _stream(stream)))
 
 
+def hs_cache_bytes(plan: Plan, capacity: int) -> int:
+    b = _sz()
+    _check(_lib.hs_cache_bytes(plan.handle, capacity, ctypes.byref(b)))
+    return int(b.value)
+
+
+def hs_cache_reset(plan: Plan, cache, capacity: int, cache_bytes: Optional[int] = None,
+                   stream=None):
+    _check(_lib.hs_cache_reset(plan.handle, _ptr(cache), _ws_bytes(cache, cache_bytes), capacity,
+                               _stream(stream)))
+
+
+def hs_cache_lookup(plan: Plan, cache, capacity: int, unique_keys, first_index, n_unique: int,
+                    n_unique_dev, topk_score, topk_index, miss_pos, miss_first, n_miss_dev,
+                    cache_bytes: Optional[int] = None, stream=None):
+    _check(_lib.hs_cache_lookup(plan.handle, _ptr(cache), _ws_bytes(cache, cache_bytes), capacity,
+                                _ptr(unique_keys), _ptr(first_index), n_unique,
+                                _ptr(n_unique_dev), _ptr(topk_score), _ptr(topk_index),
+                                _ptr(miss_pos), _ptr(miss_first), _ptr(n_miss_dev),
+                                _stream(stream)))
+
+
+def hs_cache_insert(plan: Plan, cache, capacity: int, unique_keys, miss_pos, n_unique: int,
+                    n_unique_dev, topk_score, topk_index, cache_bytes: Optional[int] = None,
+                    stream=None):
+    _check(_lib.hs_cache_insert(plan.handle, _ptr(cache), _ws_bytes(cache, cache_bytes), capacity,
+                                _ptr(unique_keys), _ptr(miss_pos), n_unique, _ptr(n_unique_dev),
+                                _ptr(topk_score), _ptr(topk_index), _stream(stream)))
+
+
 # ---------------------------------------------------------------- composition
 
 class MergedRetrieval:
@@ -252,4 +291,48 @@ class MergedRetrieval:
         self.gather_queries(q_req, stream)
         self.score_partial(corpus, scale, n_unique, stream)
         self.topk_merge(n_unique, stream)
+        self.deliver(stream)
+
+    # ------------------------------------------------ cross-window reuse
+
+    def enable_cache(self, capacity: int, stream=None):
+        """Allocates and empties a result store of `capacity` entries (a
+        power of two) and the per-window miss buffers of run_cached."""
+        import torch
+        dev = self.ws.device
+        self.cache_capacity = capacity
+        self.cache = torch.empty(max(hs_cache_bytes(self.plan, capacity), 256), dtype=torch.uint8,
+                                 device=dev)
+        c1 = max(self.cap, 1)
+        self.miss_pos = torch.empty(c1, dtype=torch.int32, device=dev)
+        self.miss_first = torch.empty(c1, dtype=torch.int32, device=dev)
+        self.n_miss = torch.zeros(1, dtype=torch.int64, device=dev)
+        self.q_miss = torch.empty_like(self.q_unique)
+        self.miss_score = torch.empty_like(self.topk_score)
+        self.miss_index = torch.empty_like(self.topk_index)
+        hs_cache_reset(self.plan, self.cache, capacity, stream=stream)
+
+    def run_cached(self, keys, q_req, corpus, scale=None, stream=None):
+        """The whole window with reuse of earlier windows' results: dedup ->
+        store lookup (hit rows filled) -> representative rows of the misses ->
+        score/top-k of the misses -> miss rows put in place -> store insert ->
+        delivery.  Distinct and miss counts stay on the device."""
+        self.dedup(keys, stream)
+        hs_cache_lookup(self.plan, self.cache, self.cache_capacity, self.unique_keys,
+                        self.first_index, -1, self.n_unique, self.topk_score, self.topk_index,
+                        self.miss_pos, self.miss_first, self.n_miss, stream=stream)
+        hs_scatter(q_req, self.R, self.q_row_bytes, self.miss_first, 0, self.cap, self.n_miss,
+                   self.q_miss, stream=stream)
+        hs_score_partial(self.plan, self.q_miss, -1, self.n_miss, corpus, scale, self.ws,
+                         stream=stream)
+        hs_topk_merge(self.plan, -1, self.n_miss, self.miss_score, self.miss_index, self.ws,
+                      stream=stream)
+        row = self.k * 4
+        hs_scatter(self.miss_score, self.cap, row, self.miss_pos, 0, self.cap, self.n_unique,
+                   self.topk_score, stream=stream)
+        hs_scatter(self.miss_index, self.cap, row, self.miss_pos, 0, self.cap, self.n_unique,
+                   self.topk_index, stream=stream)
+        hs_cache_insert(self.plan, self.cache, self.cache_capacity, self.unique_keys,
+                        self.miss_pos, -1, self.n_unique, self.topk_score, self.topk_index,
+                        stream=stream)
         self.deliver(stream)

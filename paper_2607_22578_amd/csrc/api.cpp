@@ -27,6 +27,16 @@ hipError_t launch_score_partial(const void *q, const void *corpus, const float *
 hipError_t launch_topk_merge(const void *part, int64_t n_unique, const int64_t *nu_dev,
                              int64_t cap, int64_t N, int k, int corpus_dtype, float *out_s,
                              int32_t *out_i, hipStream_t st);
+struct CacheView;
+size_t cache_layout(int64_t C, int k, void *base, CacheView *v);
+hipError_t launch_cache_reset(void *cache, int64_t C, int k, hipStream_t st);
+hipError_t launch_cache_lookup(void *cache, int64_t C, int k, const int64_t *uk,
+                               const int32_t *fi, int64_t n_unique, const int64_t *nu_dev,
+                               int64_t cap, float *out_s, int32_t *out_i, int32_t *miss_pos,
+                               int32_t *miss_first, int64_t *n_miss, hipStream_t st);
+hipError_t launch_cache_insert(void *cache, int64_t C, int k, const int64_t *uk, int64_t n_unique,
+                               const int64_t *nu_dev, int64_t cap, const int32_t *miss_pos,
+                               const float *top_s, const int32_t *top_i, hipStream_t st);
 }  // namespace hs
 
 struct hs_plan {
@@ -263,6 +273,81 @@ hs_status hs_scatter(const void *src, int64_t src_rows, int64_t row_bytes, const
   hipError_t e = hs::launch_gather(src, src_rows, row_bytes, index, index_is_i64, n_out,
                                    n_out_dev, dst, (hipStream_t)stream);
   return device_status(e, "hs_scatter launch");
+}
+
+// ---------------------------------------------------------------- result store
+
+static hs_status check_cache(const hs_plan *plan, const void *cache, size_t cache_bytes,
+                             int64_t capacity, const char *who) {
+  if (!plan) return fail(HS_ERR_INVALID_ARG, "%s: null plan", who);
+  if (capacity < 1 || capacity > ((int64_t)1 << 30) || (capacity & (capacity - 1)) != 0)
+    return fail(HS_ERR_INVALID_ARG, "%s: capacity %lld must be a power of two in [1, 2^30]", who,
+                (long long)capacity);
+  if (!cache) return fail(HS_ERR_INVALID_ARG, "%s: null cache", who);
+  if (!aligned(cache, 256)) return fail(HS_ERR_ALIGNMENT, "%s: cache not 256-byte aligned", who);
+  const size_t need = hs::cache_layout(capacity, plan->d.k, nullptr, nullptr);
+  if (cache_bytes < need)
+    return fail(HS_ERR_WORKSPACE, "%s: cache has %zu bytes, needs %zu", who, cache_bytes, need);
+  return ok();
+}
+
+hs_status hs_cache_bytes(const hs_plan *plan, int64_t capacity, size_t *bytes) {
+  if (!plan || !bytes) return fail(HS_ERR_INVALID_ARG, "hs_cache_bytes: null argument");
+  if (capacity < 1 || capacity > ((int64_t)1 << 30) || (capacity & (capacity - 1)) != 0)
+    return fail(HS_ERR_INVALID_ARG, "hs_cache_bytes: capacity %lld must be a power of two in "
+                "[1, 2^30]", (long long)capacity);
+  *bytes = hs::cache_layout(capacity, plan->d.k, nullptr, nullptr);
+  return ok();
+}
+
+hs_status hs_cache_reset(const hs_plan *plan, void *cache, size_t cache_bytes, int64_t capacity,
+                         void *stream) {
+  hs_status s = check_cache(plan, cache, cache_bytes, capacity, "hs_cache_reset");
+  if (s != HS_OK) return s;
+  hipError_t e = hs::launch_cache_reset(cache, capacity, plan->d.k, (hipStream_t)stream);
+  return device_status(e, "hs_cache_reset launch");
+}
+
+hs_status hs_cache_lookup(const hs_plan *plan, void *cache, size_t cache_bytes, int64_t capacity,
+                          const int64_t *unique_keys, const int32_t *first_index,
+                          int64_t n_unique, const int64_t *n_unique_dev, float *topk_score,
+                          int32_t *topk_index, int32_t *miss_pos, int32_t *miss_first,
+                          int64_t *n_miss_dev, void *stream) {
+  hs_status s = check_cache(plan, cache, cache_bytes, capacity, "hs_cache_lookup");
+  if (s != HS_OK) return s;
+  s = check_nu(plan, n_unique, n_unique_dev, "hs_cache_lookup");
+  if (s != HS_OK) return s;
+  if (!unique_keys || !first_index || !topk_score || !topk_index || !miss_pos || !miss_first ||
+      !n_miss_dev)
+    return fail(HS_ERR_INVALID_ARG, "hs_cache_lookup: null argument");
+  if (!aligned(unique_keys, 8) || !aligned(n_miss_dev, 8) || !aligned(first_index, 4) ||
+      !aligned(topk_score, 4) || !aligned(topk_index, 4) || !aligned(miss_pos, 4) ||
+      !aligned(miss_first, 4))
+    return fail(HS_ERR_ALIGNMENT, "hs_cache_lookup: misaligned pointer");
+  hipError_t e = hs::launch_cache_lookup(cache, capacity, plan->d.k, unique_keys, first_index,
+                                         n_unique, n_unique_dev, plan->cap, topk_score,
+                                         topk_index, miss_pos, miss_first, n_miss_dev,
+                                         (hipStream_t)stream);
+  return device_status(e, "hs_cache_lookup launch");
+}
+
+hs_status hs_cache_insert(const hs_plan *plan, void *cache, size_t cache_bytes, int64_t capacity,
+                          const int64_t *unique_keys, const int32_t *miss_pos, int64_t n_unique,
+                          const int64_t *n_unique_dev, const float *topk_score,
+                          const int32_t *topk_index, void *stream) {
+  hs_status s = check_cache(plan, cache, cache_bytes, capacity, "hs_cache_insert");
+  if (s != HS_OK) return s;
+  s = check_nu(plan, n_unique, n_unique_dev, "hs_cache_insert");
+  if (s != HS_OK) return s;
+  if (!unique_keys || !miss_pos || !topk_score || !topk_index)
+    return fail(HS_ERR_INVALID_ARG, "hs_cache_insert: null argument");
+  if (!aligned(unique_keys, 8) || !aligned(miss_pos, 4) || !aligned(topk_score, 4) ||
+      !aligned(topk_index, 4))
+    return fail(HS_ERR_ALIGNMENT, "hs_cache_insert: misaligned pointer");
+  hipError_t e = hs::launch_cache_insert(cache, capacity, plan->d.k, unique_keys, n_unique,
+                                         n_unique_dev, plan->cap, miss_pos, topk_score,
+                                         topk_index, (hipStream_t)stream);
+  return device_status(e, "hs_cache_insert launch");
 }
 
 }  // extern "C"

@@ -257,3 +257,29 @@ def expected_unique(cfg: Config) -> float:
     p = r ** (-cfg.zipf_s)
     p /= p.sum()
     return float(np.sum(1.0 - (1.0 - p) ** cfg.n_requests))
+
+
+def window_stream(name: str, n_windows: int, seed: Optional[int] = None,
+                  threads: Optional[int] = None) -> list:
+    """Successive merge windows of one workload's traffic: each window draws
+    its own Zipf sample of template ids (stream S_ZIPF * 1000 + w) over the
+    same templates, so hot templates recur across windows with the same key
+    and query row.  Returns one Workload per window, without a corpus."""
+    cfg = CONFIGS[name]
+    if cfg.dedup_only or cfg.zipf_s == 0.0:
+        raise ValueError(f"{name}: window streams need a Zipf retrieval workload")
+    if seed is None:
+        seed = BASE_SEED + ORDER.index(name)
+    perm = permutation(seed, S_PERM, cfg.n_templates)
+    offsets = np.arange(cfg.n_workflows + 1, dtype=np.int64) * cfg.per_workflow
+    out = []
+    for w in range(n_windows):
+        ranks = zipf_ranks(seed, S_ZIPF * 1000 + w, cfg.n_templates, cfg.zipf_s,
+                           cfg.n_requests)
+        tids = perm[ranks]
+        keys = template_keys(seed, tids)
+        q_req, _ = gaussian_rows(seed, S_QUERY, 0, cfg.dim, cfg.q_enc, row_ids=tids,
+                                 threads=threads)
+        out.append(Workload(cfg, seed, keys, tids, offsets, q_req, None, None,
+                            n_corpus=cfg.n_corpus, extra={"window": w}))
+    return out

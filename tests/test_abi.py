@@ -130,3 +130,41 @@ def test_scatter_validation():
     assert e.value.status == hs.HS_ERR_INVALID_ARG
     # empty work is a no-op that never touches the device
     hs.hs_scatter(FAKE, 10, 8, FAKE, 0, 0, None, FAKE)
+
+
+def test_cache_validation():
+    p = hs.hs_merge_plan(**GOOD)
+    assert hs.hs_cache_bytes(p, 1) >= 8 + 4 + 4 + 2 * 10 * 4
+    b = hs.hs_cache_bytes(p, 4096)
+    assert b >= 4096 * (16 + 80) and b % 256 == 0
+    for bad in (0, 3, 6000, -4, 2 ** 31):
+        with pytest.raises(hs.HsError) as e:
+            hs.hs_cache_bytes(p, bad)
+        assert e.value.status == hs.HS_ERR_INVALID_ARG
+    with pytest.raises(hs.HsError) as e:        # store buffer too small
+        hs.hs_cache_reset(p, FAKE, 4096, cache_bytes=b - 1)
+    assert e.value.status == hs.HS_ERR_WORKSPACE
+    with pytest.raises(hs.HsError) as e:        # misaligned store
+        hs.hs_cache_reset(p, FAKE + 16, 4096, cache_bytes=b)
+    assert e.value.status == hs.HS_ERR_ALIGNMENT
+    with pytest.raises(hs.HsError) as e:        # capacity not a power of two
+        hs.hs_cache_reset(p, FAKE, 4095, cache_bytes=b)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    with pytest.raises(hs.HsError) as e:        # n_unique beyond the plan
+        hs.hs_cache_lookup(p, FAKE, 4096, FAKE, FAKE, 4096, None, FAKE, FAKE, FAKE, FAKE, FAKE,
+                           cache_bytes=b)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    with pytest.raises(hs.HsError) as e:        # null miss count
+        hs.hs_cache_lookup(p, FAKE, 4096, FAKE, FAKE, 10, None, FAKE, FAKE, FAKE, FAKE, None,
+                           cache_bytes=b)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    with pytest.raises(hs.HsError) as e:        # misaligned keys
+        hs.hs_cache_lookup(p, FAKE, 4096, FAKE + 4, FAKE, 10, None, FAKE, FAKE, FAKE, FAKE,
+                           FAKE, cache_bytes=b)
+    assert e.value.status == hs.HS_ERR_ALIGNMENT
+    with pytest.raises(hs.HsError) as e:        # -1 without a device count
+        hs.hs_cache_insert(p, FAKE, 4096, FAKE, FAKE, -1, None, FAKE, FAKE, cache_bytes=b)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    with pytest.raises(hs.HsError) as e:
+        hs.hs_cache_insert(p, FAKE, 4096, FAKE, None, 10, None, FAKE, FAKE, cache_bytes=b)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
