@@ -312,19 +312,24 @@ class MergedRetrieval:
         self.miss_index = torch.empty_like(self.topk_index)
         hs_cache_reset(self.plan, self.cache, capacity, stream=stream)
 
-    def run_cached(self, keys, q_req, corpus, scale=None, stream=None):
+    def run_cached(self, keys, q_req, corpus, scale=None, stream=None, score_events=None):
         """The whole window with reuse of earlier windows' results: dedup ->
         store lookup (hit rows filled) -> representative rows of the misses ->
         score/top-k of the misses -> miss rows put in place -> store insert ->
-        delivery.  Distinct and miss counts stay on the device."""
+        delivery.  Distinct and miss counts stay on the device.  score_events
+        = (start, end) events recorded around the score step, if given."""
         self.dedup(keys, stream)
         hs_cache_lookup(self.plan, self.cache, self.cache_capacity, self.unique_keys,
                         self.first_index, -1, self.n_unique, self.topk_score, self.topk_index,
                         self.miss_pos, self.miss_first, self.n_miss, stream=stream)
         hs_scatter(q_req, self.R, self.q_row_bytes, self.miss_first, 0, self.cap, self.n_miss,
                    self.q_miss, stream=stream)
+        if score_events is not None:
+            score_events[0].record(stream)
         hs_score_partial(self.plan, self.q_miss, -1, self.n_miss, corpus, scale, self.ws,
                          stream=stream)
+        if score_events is not None:
+            score_events[1].record(stream)
         hs_topk_merge(self.plan, -1, self.n_miss, self.miss_score, self.miss_index, self.ws,
                       stream=stream)
         row = self.k * 4
