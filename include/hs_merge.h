@@ -22,7 +22,8 @@
  *                  Eq. 2; top-K vector retrieval of the RAG workloads, Sec. 4.1)
  *                  = hs_score_partial followed by hs_topk_merge.
  * Optionally, hs_cache_lookup / hs_cache_insert reuse results across windows
- * (Sec. 3.3 (II)), so that only keys not seen before are scored.
+ * (Sec. 3.3 (II)), so that only keys not seen before are scored, and
+ * hs_signature computes the keys themselves from node descriptions (Eq. 2).
  *
  * Conventions (all entry points):
  *   - Every function returns hs_status.  Arguments are validated on the host
@@ -215,6 +216,49 @@ hs_status hs_cache_insert(const hs_plan *plan, void *cache, size_t cache_bytes, 
                           const int64_t *unique_keys, const int32_t *miss_pos, int64_t n_unique,
                           const int64_t *n_unique_dev, const float *topk_score,
                           const int32_t *topk_index, void *stream);
+
+/* Node signatures (Eq. 2; SHA-256 as in the paper's prototype, Sec. 4.1).
+ * Sig(v) = SHA-256 of the message, all integers little-endian,
+ *     le32(tau_v) | le32(|Theta|) | Theta | le32(|D|) | D | le32(m) |
+ *     Sig(u_1) | ... | Sig(u_m)
+ * with tau_v the operator type, Theta the bytes of the parameters that affect
+ * the node's result (e.g. Top-K), D the node's input text (normalised when
+ * HS_SIG_NORMALIZE_TEXT is set: ASCII A-Z folded to a-z, every run of ASCII
+ * whitespace -- space, \t, \n, \v, \f, \r -- replaced by one space, leading
+ * and trailing whitespace dropped, all other bytes unchanged) and Sig(u_j) the
+ * 32-byte digests of the node's m predecessors in the given order.  The key
+ * that feeds hs_dedup is the digest's first 8 bytes read big-endian as a
+ * signed int64.  One call hashes nodes [first, first + count); their
+ * predecessors must have been hashed by earlier calls (ids < first), so a DAG
+ * is hashed one topological level per call on one stream.
+ * The struct is read on the host during the call; its pointers are device
+ * addresses. */
+typedef struct {
+    const uint32_t *op_type;   /* [n_nodes] tau_v */
+    const uint8_t *params;     /* Theta bytes of all nodes, concatenated */
+    const int64_t *param_off;  /* [n_nodes + 1]: node i's Theta is
+                                  params[param_off[i], param_off[i+1]); NULL = none */
+    int64_t param_bytes;       /* bytes in params, 0 <= . <= 2^32 - 16 */
+    const uint8_t *text;       /* D bytes of all nodes, concatenated */
+    const int64_t *text_off;   /* [n_nodes + 1] as param_off; NULL = empty texts */
+    int64_t text_bytes;        /* bytes in text, 0 <= . <= 2^32 - 16 */
+    const int32_t *pred_off;   /* [n_nodes + 1] into pred_idx; NULL = no predecessors */
+    const int32_t *pred_idx;   /* [pred_count] predecessor node ids, ordered */
+    int64_t pred_count;        /* 0 <= . <= 2^31 - 1 */
+    int64_t n_nodes;           /* 0 <= . <= 2^27 */
+} hs_sig_nodes;
+
+#define HS_SIG_NORMALIZE_TEXT 1
+
+/*   digest  [n_nodes x 32] bytes device, 16-byte aligned: rows < first are
+ *           read (predecessor digests), rows [first, first + count) written
+ *   keys    [n_nodes] int64 device out, may be NULL: entries
+ *           [first, first + count) written
+ * Offsets are clamped to their buffers (a range past the end is cut there, a
+ * reversed range is empty); a predecessor id outside [0, first) is hashed as
+ * 32 zero bytes.  Bit-exact and deterministic. */
+hs_status hs_signature(const hs_sig_nodes *nodes, int64_t first, int64_t count, int32_t flags,
+                       uint8_t *digest, int64_t *keys, void *stream);
 
 const char *hs_status_string(hs_status s);
 const char *hs_last_error(void);

@@ -37,7 +37,9 @@ ABI_VERSION = 1
 
 EXPORTS = ["hs_merge_plan", "hs_plan_destroy", "hs_dedup", "hs_score_topk", "hs_score_partial",
            "hs_topk_merge", "hs_scatter", "hs_cache_bytes", "hs_cache_reset", "hs_cache_lookup",
-           "hs_cache_insert", "hs_status_string", "hs_last_error", "hs_abi_version"]
+           "hs_cache_insert", "hs_signature", "hs_status_string", "hs_last_error",
+           "hs_abi_version"]
+HS_SIG_NORMALIZE_TEXT = 1
 
 
 class hs_merge_desc(ctypes.Structure):
@@ -45,6 +47,15 @@ class hs_merge_desc(ctypes.Structure):
                 ("n_corpus", ctypes.c_int64), ("k", ctypes.c_int32),
                 ("query_dtype", ctypes.c_int32), ("corpus_dtype", ctypes.c_int32),
                 ("flags", ctypes.c_int32), ("max_unique", ctypes.c_int64)]
+
+
+class hs_sig_nodes(ctypes.Structure):
+    _fields_ = [("op_type", ctypes.c_void_p), ("params", ctypes.c_void_p),
+                ("param_off", ctypes.c_void_p), ("param_bytes", ctypes.c_int64),
+                ("text", ctypes.c_void_p), ("text_off", ctypes.c_void_p),
+                ("text_bytes", ctypes.c_int64), ("pred_off", ctypes.c_void_p),
+                ("pred_idx", ctypes.c_void_p), ("pred_count", ctypes.c_int64),
+                ("n_nodes", ctypes.c_int64)]
 
 
 _vp, _i64, _i32, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
@@ -71,6 +82,8 @@ _lib.hs_cache_lookup.argtypes = [_vp, _vp, _sz, _i64, _vp, _vp, _i64] + [_vp] * 
 _lib.hs_cache_lookup.restype = ctypes.c_int
 _lib.hs_cache_insert.argtypes = [_vp, _vp, _sz, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp]
 _lib.hs_cache_insert.restype = ctypes.c_int
+_lib.hs_signature.argtypes = [ctypes.POINTER(hs_sig_nodes), _i64, _i64, _i32, _vp, _vp, _vp]
+_lib.hs_signature.restype = ctypes.c_int
 _lib.hs_status_string.argtypes = [ctypes.c_int]
 _lib.hs_status_string.restype = ctypes.c_char_p
 _lib.hs_last_error.argtypes = []
@@ -227,6 +240,28 @@ def hs_cache_insert(plan: Plan, cache, capacity: int, unique_keys, miss_pos, n_u
     _check(_lib.hs_cache_insert(plan.handle, _ptr(cache), _ws_bytes(cache, cache_bytes), capacity,
                                 _ptr(unique_keys), _ptr(miss_pos), n_unique, _ptr(n_unique_dev),
                                 _ptr(topk_score), _ptr(topk_index), _stream(stream)))
+
+
+def _nbytes(x):
+    if x is None or isinstance(x, int):
+        return 0
+    return x.numel() * x.element_size()
+
+
+def hs_signature(op_type, n_nodes: int, first: int, count: int, digest, keys=None, params=None,
+                 param_off=None, text=None, text_off=None, pred_off=None, pred_idx=None,
+                 flags: int = 0, param_bytes: Optional[int] = None,
+                 text_bytes: Optional[int] = None, pred_count: Optional[int] = None,
+                 stream=None):
+    """Signatures of nodes [first, first + count) (digests and 64-bit keys);
+    buffer sizes default to the tensors' sizes."""
+    nd = hs_sig_nodes(_ptr(op_type), _ptr(params), _ptr(param_off),
+                      _nbytes(params) if param_bytes is None else param_bytes,
+                      _ptr(text), _ptr(text_off), _nbytes(text) if text_bytes is None else text_bytes,
+                      _ptr(pred_off), _ptr(pred_idx),
+                      (_nbytes(pred_idx) // 4) if pred_count is None else pred_count, n_nodes)
+    _check(_lib.hs_signature(ctypes.byref(nd), first, count, flags, _ptr(digest), _ptr(keys),
+                             _stream(stream)))
 
 
 # ---------------------------------------------------------------- composition

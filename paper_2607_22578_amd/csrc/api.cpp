@@ -37,6 +37,12 @@ hipError_t launch_cache_lookup(void *cache, int64_t C, int k, const int64_t *uk,
 hipError_t launch_cache_insert(void *cache, int64_t C, int k, const int64_t *uk, int64_t n_unique,
                                const int64_t *nu_dev, int64_t cap, const int32_t *miss_pos,
                                const float *top_s, const int32_t *top_i, hipStream_t st);
+hipError_t launch_signature(const uint32_t *op_type, const uint8_t *params,
+                            const int64_t *param_off, int64_t param_bytes, const uint8_t *text,
+                            const int64_t *text_off, int64_t text_bytes, const int32_t *pred_off,
+                            const int32_t *pred_idx, int64_t pred_count, int64_t first,
+                            int64_t count, int normalize, uint8_t *digest, int64_t *keys,
+                            hipStream_t st);
 }  // namespace hs
 
 struct hs_plan {
@@ -348,6 +354,44 @@ hs_status hs_cache_insert(const hs_plan *plan, void *cache, size_t cache_bytes, 
                                          n_unique_dev, plan->cap, miss_pos, topk_score,
                                          topk_index, (hipStream_t)stream);
   return device_status(e, "hs_cache_insert launch");
+}
+
+// ---------------------------------------------------------------- signatures
+
+hs_status hs_signature(const hs_sig_nodes *nd, int64_t first, int64_t count, int32_t flags,
+                       uint8_t *digest, int64_t *keys, void *stream) {
+  if (!nd) return fail(HS_ERR_INVALID_ARG, "hs_signature: null node description");
+  const int64_t kMaxBuf = ((int64_t)1 << 32) - 16;
+  if (nd->n_nodes < 0 || nd->n_nodes > ((int64_t)1 << 27))
+    return fail(HS_ERR_INVALID_ARG, "hs_signature: n_nodes %lld out of [0, 2^27]",
+                (long long)nd->n_nodes);
+  if (first < 0 || count < 0 || first > nd->n_nodes - count)
+    return fail(HS_ERR_INVALID_ARG, "hs_signature: range [%lld, +%lld) outside [0, %lld)",
+                (long long)first, (long long)count, (long long)nd->n_nodes);
+  if ((flags & ~HS_SIG_NORMALIZE_TEXT) != 0)
+    return fail(HS_ERR_INVALID_ARG, "hs_signature: unknown flags 0x%x", flags);
+  if (nd->param_bytes < 0 || nd->param_bytes > kMaxBuf || nd->text_bytes < 0 ||
+      nd->text_bytes > kMaxBuf)
+    return fail(HS_ERR_INVALID_ARG, "hs_signature: buffer sizes must be in [0, 2^32 - 16]");
+  if (nd->pred_count < 0 || nd->pred_count > INT32_MAX)
+    return fail(HS_ERR_INVALID_ARG, "hs_signature: pred_count out of [0, 2^31 - 1]");
+  if (count == 0) return ok();
+  if (!nd->op_type || !digest)
+    return fail(HS_ERR_INVALID_ARG, "hs_signature: null op_type or digest");
+  if ((nd->param_off && nd->param_bytes > 0 && !nd->params) ||
+      (nd->text_off && nd->text_bytes > 0 && !nd->text) ||
+      (nd->pred_off && nd->pred_count > 0 && !nd->pred_idx))
+    return fail(HS_ERR_INVALID_ARG, "hs_signature: null data buffer with a non-zero size");
+  if (!aligned(digest, 16) || !aligned(keys, 8) || !aligned(nd->op_type, 4) ||
+      !aligned(nd->param_off, 8) || !aligned(nd->text_off, 8) || !aligned(nd->pred_off, 4) ||
+      !aligned(nd->pred_idx, 4))
+    return fail(HS_ERR_ALIGNMENT, "hs_signature: misaligned pointer");
+  hipError_t e = hs::launch_signature(
+      nd->op_type, nd->params, nd->param_off, nd->params ? nd->param_bytes : 0, nd->text,
+      nd->text_off, nd->text ? nd->text_bytes : 0, nd->pred_off, nd->pred_idx,
+      nd->pred_idx ? nd->pred_count : 0, first, count, (flags & HS_SIG_NORMALIZE_TEXT) ? 1 : 0,
+      digest, keys, (hipStream_t)stream);
+  return device_status(e, "hs_signature launch");
 }
 
 }  // extern "C"

@@ -1,0 +1,344 @@
+// Node semantic signatures on the device.
+//
+// HeraSys Eq. 2: a node's signature hashes its operator type tau_v, the
+// parameters that affect its result Theta_p, the input data D_in that fixes
+// its output (for retrieval and embedding nodes, the normalised query text or
+// the chunk content) and the ordered signatures of its predecessors.  The
+// prototype hashes with SHA-256 (Sec. 4.1, testbed).  The message of node v is
+// the length-prefixed concatenation (all integers little-endian)
+//
+//   le32(tau_v) | le32(|Theta|) | Theta | le32(|D|) | D | le32(m) |
+//   Sig(u_1) | ... | Sig(u_m)
+//
+// where D is the node's text, normalised or not, and Sig(u_j) are the 32-byte
+// digests of the m predecessors in their given order.  The length prefixes
+// make the encoding injective.  Normalisation folds ASCII A-Z to a-z,
+// replaces each run of ASCII whitespace (space, \t, \n, \v, \f, \r) by one
+// space and drops leading and trailing whitespace; other bytes pass through.
+// The 64-bit key that feeds the dedup is the digest's first 8 bytes read
+// big-endian, as a signed (two's-complement) integer.
+//
+// One thread per node: SHA-256 is sequential within a message, and a window
+// holds thousands of nodes.  The thread streams its message bytes through a
+// 16-word shift register (static register indexing only) and compresses every
+// 64 bytes (FIPS 180-4, Sec. 6.2).  Byte sources are read 16 bytes at a time
+// through buffer descriptors, so reads past a buffer's end return zeros and
+// never touch memory.
+#include "common.h"
+
+namespace hs {
+
+typedef int i32x4s __attribute__((ext_vector_type(4)));
+
+// FIPS 180-4 Sec. 4.2.2: first 32 bits of the fractional parts of the cube
+// roots of the first 64 primes.
+__device__ constexpr uint32_t kSha256K[64] = {
+    0x428a2f98u, 0x71374491u, 0xb5c0fbcfu, 0xe9b5dba5u, 0x3956c25bu, 0x59f111f1u, 0x923f82a4u,
+    0xab1c5ed5u, 0xd807aa98u, 0x12835b01u, 0x243185beu, 0x550c7dc3u, 0x72be5d74u, 0x80deb1feu,
+    0x9bdc06a7u, 0xc19bf174u, 0xe49b69c1u, 0xefbe4786u, 0x0fc19dc6u, 0x240ca1ccu, 0x2de92c6fu,
+    0x4a7484aau, 0x5cb0a9dcu, 0x76f988dau, 0x983e5152u, 0xa831c66du, 0xb00327c8u, 0xbf597fc7u,
+    0xc6e00bf3u, 0xd5a79147u, 0x06ca6351u, 0x14292967u, 0x27b70a85u, 0x2e1b2138u, 0x4d2c6dfcu,
+    0x53380d13u, 0x650a7354u, 0x766a0abbu, 0x81c2c92eu, 0x92722c85u, 0xa2bfe8a1u, 0xa81a664bu,
+    0xc24b8b70u, 0xc76c51a3u, 0xd192e819u, 0xd6990624u, 0xf40e3585u, 0x106aa070u, 0x19a4c116u,
+    0x1e376c08u, 0x2748774cu, 0x34b0bcb5u, 0x391c0cb3u, 0x4ed8aa4au, 0x5b9cca4fu, 0x682e6ff3u,
+    0x748f82eeu, 0x78a5636fu, 0x84c87814u, 0x8cc70208u, 0x90befffau, 0xa4506cebu, 0xbef9a3f7u,
+    0xc67178f2u};
+
+// FIPS 180-4 Sec. 5.3.3: first 32 bits of the fractional parts of the square
+// roots of the first 8 primes.
+__device__ constexpr uint32_t kSha256H0[8] = {0x6a09e667u, 0xbb67ae85u, 0x3c6ef372u,
+                                              0xa54ff53au, 0x510e527fu, 0x9b05688cu,
+                                              0x1f83d9abu, 0x5be0cd19u};
+
+__device__ __forceinline__ uint32_t rotr(uint32_t x, int n) {
+  return (x >> n) | (x << (32 - n));
+}
+
+// One SHA-256 block: w[0..15] are the block's words (big-endian), h the state.
+__device__ __forceinline__ void sha256_block(uint32_t h[8], uint32_t w[16]) {
+  uint32_t a = h[0], b = h[1], c = h[2], d = h[3], e = h[4], f = h[5], g = h[6], hh = h[7];
+#pragma unroll
+  for (int t = 0; t < 64; ++t) {
+    if (t >= 16) {   // message schedule in a rolling 16-word window
+      const uint32_t w15 = w[(t - 15) & 15], w2 = w[(t - 2) & 15];
+      const uint32_t s0 = rotr(w15, 7) ^ rotr(w15, 18) ^ (w15 >> 3);
+      const uint32_t s1 = rotr(w2, 17) ^ rotr(w2, 19) ^ (w2 >> 10);
+      w[t & 15] = w[t & 15] + s0 + w[(t - 7) & 15] + s1;
+    }
+    const uint32_t S1 = rotr(e, 6) ^ rotr(e, 11) ^ rotr(e, 25);
+    const uint32_t ch = (e & f) ^ (~e & g);
+    const uint32_t t1 = hh + S1 + ch + kSha256K[t] + w[t & 15];
+    const uint32_t S0 = rotr(a, 2) ^ rotr(a, 13) ^ rotr(a, 22);
+    const uint32_t mj = (a & b) ^ (a & c) ^ (b & c);
+    const uint32_t t2 = S0 + mj;
+    hh = g;
+    g = f;
+    f = e;
+    e = d + t1;
+    d = c;
+    c = b;
+    b = a;
+    a = t1 + t2;
+  }
+  h[0] += a;
+  h[1] += b;
+  h[2] += c;
+  h[3] += d;
+  h[4] += e;
+  h[5] += f;
+  h[6] += g;
+  h[7] += hh;
+}
+
+// Byte at `pos` of a 16-byte window held as four little-endian words.
+__device__ __forceinline__ uint32_t win_byte(const uint32_t win[4], uint32_t pos) {
+  const uint32_t q = (pos >> 2) & 3u;
+  const uint32_t wd = q == 0 ? win[0] : q == 1 ? win[1] : q == 2 ? win[2] : win[3];
+  return (wd >> ((pos & 3u) * 8u)) & 0xffu;
+}
+
+__device__ __forceinline__ bool ascii_space(uint32_t c) {
+  return c == 0x20u || (c >= 0x09u && c <= 0x0du);
+}
+
+__device__ __forceinline__ uint32_t ascii_lower(uint32_t c) {
+  return (c >= 0x41u && c <= 0x5au) ? c + 0x20u : c;
+}
+
+// 16 bytes at the 16-aligned offset `off` of a buffer of `nbytes`; bytes past
+// the end read as zero.  The last partial block is read byte by byte (a
+// 16-byte buffer load that straddles the end may return zeros for all of it).
+__device__ __forceinline__ void load_window(__amdgpu_buffer_rsrc_t r, uint32_t off,
+                                            uint32_t nbytes, uint32_t win[4]) {
+  if (off + 16u <= nbytes) {
+    const i32x4s v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+    win[0] = (uint32_t)v[0];
+    win[1] = (uint32_t)v[1];
+    win[2] = (uint32_t)v[2];
+    win[3] = (uint32_t)v[3];
+  } else {
+    uint32_t t[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const uint32_t b =
+          off + i < nbytes ? (uint32_t)__builtin_amdgcn_raw_buffer_load_b8(r, (int)(off + i), 0, 0)
+                           : 0u;
+      t[i >> 2] |= b << ((i & 3) * 8);
+    }
+    win[0] = t[0];
+    win[1] = t[1];
+    win[2] = t[2];
+    win[3] = t[3];
+  }
+}
+
+struct SigArgs {
+  const uint32_t *op_type;
+  const uint8_t *params;
+  const int64_t *param_off;
+  uint32_t param_bytes;
+  const uint8_t *text;
+  const int64_t *text_off;
+  uint32_t text_bytes;
+  const int32_t *pred_off;
+  const int32_t *pred_idx;
+  int64_t pred_count;
+  int64_t first, count;
+  int normalize;
+  uint8_t *digest;
+  int64_t *keys;
+};
+
+__device__ __forceinline__ void clamp_range(const int64_t *off, int64_t i, uint32_t nbytes,
+                                            uint32_t &b, uint32_t &e) {
+  int64_t lo = off ? off[i] : 0, hi = off ? off[i + 1] : 0;
+  lo = lo < 0 ? 0 : lo > (int64_t)nbytes ? (int64_t)nbytes : lo;
+  hi = hi < lo ? lo : hi > (int64_t)nbytes ? (int64_t)nbytes : hi;
+  b = (uint32_t)lo;
+  e = (uint32_t)hi;
+}
+
+constexpr int kSigThreads = 256;
+
+__global__ __launch_bounds__(kSigThreads) void signature_kernel(SigArgs a) {
+  // all lanes read the same buffers: the descriptors are wave-uniform
+  const __amdgpu_buffer_rsrc_t rp =
+      __builtin_amdgcn_make_buffer_rsrc((void *)a.params, (short)0, (int)a.param_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rt =
+      __builtin_amdgcn_make_buffer_rsrc((void *)a.text, (short)0, (int)a.text_bytes, 0x00020000);
+  const uint32_t dig_bytes = (uint32_t)(a.first * 32);   // digests of earlier nodes only
+  const __amdgpu_buffer_rsrc_t rd =
+      __builtin_amdgcn_make_buffer_rsrc((void *)a.digest, (short)0, (int)dig_bytes, 0x00020000);
+
+  for (int64_t v = a.first + (int64_t)blockIdx.x * kSigThreads + threadIdx.x;
+       v < a.first + a.count; v += (int64_t)gridDim.x * kSigThreads) {
+    const uint32_t tau = a.op_type[v];
+    uint32_t p0, p1, t0, t1;
+    clamp_range(a.param_off, v, a.param_bytes, p0, p1);
+    clamp_range(a.text_off, v, a.text_bytes, t0, t1);
+    int64_t q0 = 0, q1 = 0;
+    if (a.pred_off) {
+      q0 = a.pred_off[v];
+      q1 = a.pred_off[v + 1];
+      q0 = q0 < 0 ? 0 : q0 > a.pred_count ? a.pred_count : q0;
+      q1 = q1 < q0 ? q0 : q1 > a.pred_count ? a.pred_count : q1;
+    }
+    const uint32_t P = p1 - p0, m = (uint32_t)(q1 - q0);
+    uint32_t win[4];
+
+    // pass 1: length of D
+    uint32_t D = t1 - t0;
+    if (a.normalize) {
+      D = 0;
+      bool gap = false;
+      for (uint32_t r = t0; r < t1; ++r) {
+        if (r == t0 || (r & 15u) == 0) load_window(rt, r & ~15u, a.text_bytes, win);
+        const uint32_t c = win_byte(win, r);
+        if (ascii_space(c)) {
+          gap = true;
+        } else {
+          D += (gap && D > 0) ? 2u : 1u;
+          gap = false;
+        }
+      }
+    }
+
+    // pass 2: stream the message (plus FIPS 180-4 padding) through the block
+    const uint32_t L = 16u + P + D + 32u * m;
+    const uint32_t nblk = (L + 8u) / 64u + 1u;
+    const uint32_t end = nblk * 64u;
+    const uint64_t bits = (uint64_t)L * 8u;
+    const uint32_t sP = 8u, sDl = 8u + P, sD = 12u + P, sM = 12u + P + D, sQ = 16u + P + D;
+    uint32_t h[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[i] = kSha256H0[i];
+    uint32_t w[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) w[i] = 0u;
+    uint32_t cur = 0u, nb = 0u, nw = 0u;
+    uint32_t rp_pos = p0, rt_pos = t0, wbase = 0xffffffffu;   // window state
+    int src = -1;                                            // 0 params, 1 text, 2 digests
+    bool gap = false;
+    uint32_t emitted = 0u;
+    int64_t pi = -1;   // current predecessor
+    for (uint32_t pos = 0; pos < end; ++pos) {
+      uint32_t b;
+      if (pos < sP) {
+        b = ((pos < 4u ? tau : P) >> ((pos & 3u) * 8u)) & 0xffu;
+      } else if (pos < sDl) {
+        if (src != 0 || (rp_pos & ~15u) != wbase) {
+          wbase = rp_pos & ~15u;
+          load_window(rp, wbase, a.param_bytes, win);
+          src = 0;
+        }
+        b = win_byte(win, rp_pos);
+        ++rp_pos;
+      } else if (pos < sD) {
+        b = (D >> ((pos - sDl) * 8u)) & 0xffu;
+      } else if (pos < sM) {
+        // next byte of D: raw, or normalised (a pending gap emits one space
+        // before the next non-space byte; leading spaces never emit one)
+        for (;;) {
+          if (src != 1 || (rt_pos & ~15u) != wbase) {
+            wbase = rt_pos & ~15u;
+            load_window(rt, wbase, a.text_bytes, win);
+            src = 1;
+          }
+          const uint32_t c = win_byte(win, rt_pos);
+          if (!a.normalize) {
+            b = c;
+            ++rt_pos;
+            break;
+          }
+          if (ascii_space(c)) {
+            gap = true;
+            ++rt_pos;
+            continue;
+          }
+          if (gap && emitted > 0u) {
+            b = 0x20u;   // the space; c is emitted next time
+            gap = false;
+          } else {
+            b = ascii_lower(c);
+            gap = false;
+            ++rt_pos;
+          }
+          break;
+        }
+        ++emitted;
+      } else if (pos < sQ) {
+        b = (m >> ((pos - sM) * 8u)) & 0xffu;
+      } else if (pos < L) {
+        const uint32_t j = pos - sQ;
+        if ((j & 31u) == 0u) pi = a.pred_idx[q0 + (j >> 5)];
+        if (pi >= 0 && pi < a.first) {
+          const uint32_t off = (uint32_t)pi * 32u + (j & 31u);
+          if (src != 2 || (off & ~15u) != wbase) {
+            wbase = off & ~15u;
+            load_window(rd, wbase, dig_bytes, win);
+            src = 2;
+          }
+          b = win_byte(win, off);
+        } else {
+          b = 0u;   // a predecessor outside [0, first) hashes as 32 zero bytes
+        }
+      } else if (pos == L) {
+        b = 0x80u;
+      } else if (pos >= end - 8u) {
+        b = (uint32_t)(bits >> ((end - 1u - pos) * 8u)) & 0xffu;
+      } else {
+        b = 0u;
+      }
+      cur = (cur << 8) | b;
+      if (++nb == 4u) {
+#pragma unroll
+        for (int i = 0; i < 15; ++i) w[i] = w[i + 1];
+        w[15] = cur;
+        cur = 0u;
+        nb = 0u;
+        if (++nw == 16u) {
+          sha256_block(h, w);
+          nw = 0u;
+        }
+      }
+    }
+
+    uint4 *dst = (uint4 *)(a.digest + v * 32);
+    dst[0] = make_uint4(__builtin_bswap32(h[0]), __builtin_bswap32(h[1]),
+                        __builtin_bswap32(h[2]), __builtin_bswap32(h[3]));
+    dst[1] = make_uint4(__builtin_bswap32(h[4]), __builtin_bswap32(h[5]),
+                        __builtin_bswap32(h[6]), __builtin_bswap32(h[7]));
+    if (a.keys) a.keys[v] = (int64_t)(((uint64_t)h[0] << 32) | h[1]);
+  }
+}
+
+hipError_t launch_signature(const uint32_t *op_type, const uint8_t *params,
+                            const int64_t *param_off, int64_t param_bytes, const uint8_t *text,
+                            const int64_t *text_off, int64_t text_bytes, const int32_t *pred_off,
+                            const int32_t *pred_idx, int64_t pred_count, int64_t first,
+                            int64_t count, int normalize, uint8_t *digest, int64_t *keys,
+                            hipStream_t st) {
+  if (count <= 0) return hipSuccess;
+  SigArgs a;
+  a.op_type = op_type;
+  a.params = params;
+  a.param_off = param_off;
+  a.param_bytes = (uint32_t)param_bytes;
+  a.text = text;
+  a.text_off = text_off;
+  a.text_bytes = (uint32_t)text_bytes;
+  a.pred_off = pred_off;
+  a.pred_idx = pred_idx;
+  a.pred_count = pred_count;
+  a.first = first;
+  a.count = count;
+  a.normalize = normalize;
+  a.digest = digest;
+  a.keys = keys;
+  int64_t blocks = (count + kSigThreads - 1) / kSigThreads;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(signature_kernel, dim3((unsigned)blocks), dim3(kSigThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace hs

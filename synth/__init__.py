@@ -31,6 +31,7 @@ _lib = None
 
 # named streams
 S_QUERY, S_CORPUS, S_TABLE, S_ZIPF, S_PERM, S_KEY, S_SLOTS = 1, 2, 3, 4, 5, 6, 7
+S_TEXT, S_RENDER = 8, 9
 ENC = {"f32": 0, "bf16": 1, "fp8": 2}
 BASE_SEED = 20260722
 
@@ -283,3 +284,60 @@ def window_stream(name: str, n_windows: int, seed: Optional[int] = None,
         out.append(Workload(cfg, seed, keys, tids, offsets, q_req, None, None,
                             n_corpus=cfg.n_corpus, extra={"window": w}))
     return out
+
+
+# --------------------------------------------------------------------------
+# node texts (inputs of the signature step)
+
+_WS = b" \t\n\r\x0b\x0c"
+_ACCENTED = ["\u00e9", "\u00c9", "\u00fc", "\u00df", "\u4e2d"]   # multi-byte UTF-8
+
+
+def template_text(seed: int, template_id: int) -> bytes:
+    """Canonical text of a query template: 4-15 pseudo-words of 2-10 lower-case
+    letters (some carrying a multi-byte UTF-8 letter), single spaces."""
+    g = np.random.default_rng([seed, S_TEXT, int(template_id)])
+    words = []
+    for _ in range(int(g.integers(4, 16))):
+        w = "".join(chr(97 + int(c)) for c in g.integers(0, 26, size=int(g.integers(2, 11))))
+        if g.random() < 0.05:
+            w += _ACCENTED[int(g.integers(0, len(_ACCENTED)))]
+        words.append(w)
+    return " ".join(words).encode("utf-8")
+
+
+def render_texts(seed: int, template_ids: np.ndarray, vary: bool = True):
+    """Request texts packed back to back: (uint8 buffer, int64 offsets [R+1]).
+    With `vary`, each request renders its template with its own case flips of
+    ASCII letters and runs of ASCII whitespace between, before and after the
+    words, as users type the same query differently; the normalised forms of
+    a template's renderings are identical."""
+    parts = []
+    cache = {}
+    for i, t in enumerate(np.asarray(template_ids, dtype=np.int64)):
+        t = int(t)
+        if t not in cache:
+            cache[t] = template_text(seed, t)
+        base = cache[t]
+        if not vary:
+            parts.append(base)
+            continue
+        g = np.random.default_rng([seed, S_RENDER, i])
+        out = bytearray()
+        if g.random() < 0.3:
+            out += bytes(_WS[int(c)] for c in g.integers(0, 6, size=int(g.integers(1, 4))))
+        for j, word in enumerate(base.split(b" ")):
+            if j:
+                n = int(g.integers(1, 4)) if g.random() < 0.3 else 1
+                out += bytes(_WS[int(c)] for c in g.integers(0, 6, size=n)) if n > 1 or \
+                    g.random() < 0.2 else b" "
+            flips = g.random(len(word)) < 0.15
+            out += bytes((c - 32) if (f and 97 <= c <= 122) else c for c, f in zip(word, flips))
+        if g.random() < 0.3:
+            out += bytes(_WS[int(c)] for c in g.integers(0, 6, size=int(g.integers(1, 4))))
+        parts.append(bytes(out))
+    off = np.zeros(len(parts) + 1, dtype=np.int64)
+    off[1:] = np.cumsum([len(x) for x in parts])
+    buf = np.frombuffer(b"".join(parts), dtype=np.uint8).copy()
+    return buf, off
+

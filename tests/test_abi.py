@@ -168,3 +168,26 @@ def test_cache_validation():
     with pytest.raises(hs.HsError) as e:
         hs.hs_cache_insert(p, FAKE, 4096, FAKE, None, 10, None, FAKE, FAKE, cache_bytes=b)
     assert e.value.status == hs.HS_ERR_INVALID_ARG
+
+
+def test_signature_validation():
+    def call(n=10, first=0, count=10, flags=0, digest=FAKE, keys=FAKE, **kw):
+        base = dict(op_type=FAKE, text=FAKE, text_off=FAKE, text_bytes=100)
+        base.update(kw)
+        hs.hs_signature(base.pop("op_type"), n, first, count, digest, keys, flags=flags,
+                        **base)
+
+    for bad in (dict(n=-1), dict(n=2 ** 27 + 1), dict(first=-1), dict(count=11),
+                dict(first=5, count=6), dict(flags=2), dict(text_bytes=2 ** 32),
+                dict(op_type=None), dict(digest=None), dict(text=None),
+                dict(pred_off=FAKE, pred_idx=None, pred_count=3),
+                dict(pred_off=FAKE, pred_idx=FAKE, pred_count=2 ** 31)):
+        with pytest.raises(hs.HsError) as e:
+            call(**bad)
+        assert e.value.status == hs.HS_ERR_INVALID_ARG, bad
+    for bad in (dict(digest=FAKE + 8), dict(keys=FAKE + 4), dict(op_type=FAKE + 2),
+                dict(text_off=FAKE + 4)):
+        with pytest.raises(hs.HsError) as e:
+            call(**bad)
+        assert e.value.status == hs.HS_ERR_ALIGNMENT, bad
+    call(count=0, first=10)   # empty range: nothing is enqueued
