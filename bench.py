@@ -76,6 +76,13 @@ def parse():
                     help="cross-window reuse: a result store of this many entries (a power "
                          "of two); each step is the next window of the workload's request "
                          "stream, scored only where the store misses")
+    ap.add_argument("--signatures", action="store_true",
+                    help="each step starts from node descriptions: the request keys are the "
+                         "SHA-256 signatures of the requests' texts (hs_signature), not "
+                         "precomputed")
+    ap.add_argument("--sig-nodes", type=int, default=0,
+                    help="only time hs_signature on this many request nodes of the workload's "
+                         "traffic (one JSON line of its own)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
     return ap.parse_args()
@@ -100,6 +107,9 @@ def main():
         sys.exit(2)
     if args.copy_bytes:
         copy_calibration(args.copy_bytes)
+        return
+    if args.sig_nodes:
+        signature_bench(args)
         return
 
     import numpy as np
@@ -130,6 +140,14 @@ def main():
     scale = to_dev(w.scale) if w.scale is not None else None
     m = hs.MergedRetrieval(R, d, N, k, qdt, cdt, device=dev)
     stream = torch.cuda.Stream(dev)   # default priority
+    sig = None
+    if args.signatures:
+        if args.no_merge:
+            raise SystemExit("--signatures and --no-merge exclude each other")
+        buf, off = synth.render_texts(w.seed, w.template_ids)
+        sig = SigInputs(hs, dev, buf, off, k)
+        keys = sig.keys
+    sig_ev = {}
     windows = None
     if args.reuse_store:
         # successive windows of the same traffic: window i is step i of the run
@@ -139,6 +157,12 @@ def main():
     step_no = [0]
 
     def step(ev=None):
+        if sig is not None:
+            if ev is not None:
+                sig_ev[id(ev)][0].record(stream)
+            sig.run(stream)
+            if ev is not None:
+                sig_ev[id(ev)][1].record(stream)
         if windows is not None:
             wk, wq = windows[step_no[0]]
             step_no[0] += 1
@@ -165,6 +189,9 @@ def main():
     ev_steps = list(range(0, args.steps, EV_EVERY))
     evs = {i: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for i in ev_steps}
+    for e in evs.values():
+        sig_ev[id(e)] = (torch.cuda.Event(enable_timing=True),
+                         torch.cuda.Event(enable_timing=True))
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize(dev)
@@ -219,6 +246,11 @@ def main():
         st_ev[5].record(stream)
         torch.cuda.synchronize(dev)
         acc += [st_ev[i].elapsed_time(st_ev[i + 1]) for i in range(5)]
+    sig_stats = None
+    if sig is not None:
+        sig_ms = float(np.mean([sig_ev[id(e)][0].elapsed_time(sig_ev[id(e)][1])
+                                for e in evs.values()]))
+        sig_stats = sig.stats(sig_ms)
     stages = dict(zip(["dedup", "gather", "score_partial", "topk_merge", "deliver"],
                       (acc / max(reps, 1)).round(4).tolist())) if reps else None
 
@@ -266,15 +298,112 @@ def main():
         "config": {"workload": f"{cfg.name}: {cfg.desc}", "n_requests": R, "n_unique": n_distinct,
                    "dim": d, "n_corpus": N, "k": k, "query_dtype": cfg.q_enc,
                    "corpus_dtype": cfg.c_enc, "seed": w.seed,
-                   "merge": not args.no_merge, "reuse": reuse},
+                   "merge": not args.no_merge, "reuse": reuse,
+                   "signatures": args.signatures},
         "unique_queries_per_s": round(n_distinct * args.steps / (total_ms * 1e-3), 1),
         "stages_ms": stages,
         "wall_s_timed": round(wall, 4),
         "roofline": roof,
     }
+    if sig_stats is not None:
+        out["signature_step"] = sig_stats
 
     if not args.no_cpu_baseline and windows is None:
         out["cpu_baseline"] = cpu_baseline(w, n_u, args.cpu_sample)
+    print(json.dumps(out), flush=True)
+
+
+# SHA-256 work per 64-byte block, counted from the FIPS 180-4 definitions:
+# 64 rounds of 26 operations (T1: Sigma1 5, Ch 4, 4 additions; T2: Sigma0 5,
+# Maj 5, 1 addition; e and a: 2 additions), 48 schedule words of 13 (two sigma
+# functions of 5, 3 additions) and 8 final additions.
+SHA_OPS_PER_BLOCK = 64 * 26 + 48 * 13 + 8
+# 32-bit integer VALU peak: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+PEAK_INT32_OPS = 256 * 4 * 16 * 2.4e9
+
+
+def _normalised_len(t: bytes) -> int:
+    return len(b" ".join(t.lower().split()))
+
+
+class SigInputs:
+    """Device buffers of one window's request nodes for hs_signature:
+    retrieval nodes (operator type 2) with Top-K as their parameter bytes and
+    their query text, normalised; no predecessors."""
+
+    def __init__(self, hs, dev, buf, off, k):
+        import numpy as np
+        import torch
+        self.hs = hs
+        n = len(off) - 1
+        self.n = n
+        self.op = torch.full((n,), 2, dtype=torch.int32, device=dev)
+        self.par = torch.from_numpy(np.full(n, k, dtype=np.uint32).view(np.uint8).copy()).to(dev)
+        self.poff = torch.arange(0, 4 * (n + 1), 4, dtype=torch.int64, device=dev)
+        self.text = torch.from_numpy(buf if buf.size else np.zeros(1, np.uint8)).to(dev)
+        self.text_bytes = int(buf.size)
+        self.toff = torch.from_numpy(off).to(dev)
+        self.digest = torch.empty((max(n, 1), 32), dtype=torch.uint8, device=dev)
+        self.keys = torch.empty(max(n, 1), dtype=torch.int64, device=dev)
+        raw = buf.tobytes()
+        lens = [16 + 4 + _normalised_len(raw[off[i]:off[i + 1]]) for i in range(n)]
+        self.blocks = int(sum((L + 8) // 64 + 1 for L in lens))
+        self.msg_bytes = int(sum(lens))
+
+    def run(self, stream):
+        self.hs.hs_signature(self.op, self.n, 0, self.n, self.digest, self.keys, params=self.par,
+                             param_off=self.poff, text=self.text, text_off=self.toff,
+                             text_bytes=self.text_bytes, flags=self.hs.HS_SIG_NORMALIZE_TEXT,
+                             stream=stream)
+
+    def stats(self, ms: float) -> dict:
+        ops = self.blocks * SHA_OPS_PER_BLOCK
+        t = ms * 1e-3
+        return {"kernel": "signature_kernel", "nodes": self.n, "text_bytes": self.text_bytes,
+                "message_bytes": self.msg_bytes, "sha256_blocks": self.blocks,
+                "kernel_ms": round(ms, 4), "nodes_per_s": round(self.n / t, 1),
+                "roofline": {"bound": "alu", "achieved": round(ops / t / 1e12, 4),
+                             "peak": PEAK_INT32_OPS / 1e12, "unit": "Tops/s",
+                             "frac": round(ops / t / PEAK_INT32_OPS, 4),
+                             "ops_per_block": SHA_OPS_PER_BLOCK}}
+
+
+def signature_bench(args):
+    """hs_signature alone on `--sig-nodes` request nodes drawn like the
+    workload's requests (Zipf template ids, per-request renderings)."""
+    import numpy as np
+    import torch
+
+    import paper_2607_22578_amd as hs
+    import synth
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = synth.CONFIGS[args.workload]
+    seed = synth.BASE_SEED + synth.ORDER.index(args.workload)
+    ranks = synth.zipf_ranks(seed, synth.S_ZIPF, cfg.n_templates, cfg.zipf_s, args.sig_nodes)
+    tids = synth.permutation(seed, synth.S_PERM, cfg.n_templates)[ranks]
+    buf, off = synth.render_texts(seed, tids)
+    sig = SigInputs(hs, dev, buf, off, max(cfg.k, 1))
+    stream = torch.cuda.Stream(dev)
+    for _ in range(args.warmup):
+        sig.run(stream)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize(dev)
+    a.record(stream)
+    for _ in range(args.steps):
+        sig.run(stream)
+    b.record(stream)
+    torch.cuda.synchronize(dev)
+    ms = a.elapsed_time(b) / args.steps
+    st = sig.stats(ms)
+    out = {"metric": "node signatures/s (SHA-256 of Eq. 2 messages)", "value": st["nodes_per_s"],
+           "unit": "nodes/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "u32", "data": "synthetic",
+           "config": {"workload": f"{args.sig_nodes} request nodes of {cfg.name}'s traffic "
+                                  f"(Zipf({cfg.zipf_s}) over {cfg.n_templates} templates), "
+                                  "normalised query text + Top-K parameter"},
+           "roofline": st["roofline"], "signature_step": st}
     print(json.dumps(out), flush=True)
 
 

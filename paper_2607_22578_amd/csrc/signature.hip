@@ -158,8 +158,62 @@ __device__ __forceinline__ void clamp_range(const int64_t *off, int64_t i, uint3
   e = (uint32_t)hi;
 }
 
-constexpr int kSigThreads = 256;
+constexpr int kSigThreads = 128;
+// LDS staging of one group's text and parameter bytes
+constexpr uint32_t kStageText = 16 * 1024, kStageParam = 2 * 1024;
+// Messages of at most kMsgMax bytes (three blocks with the padding) are built
+// whole in LDS, one column of kMsgWords words per thread, and compressed from
+// there; longer ones are streamed.
+constexpr uint32_t kMsgWords = 48, kMsgMax = kMsgWords * 4 - 9;
 
+// Stages [sb, sb + sl) of a buffer of `nbytes` (sb, sl multiples of 16) into
+// LDS with coalesced 16-byte loads, eight in flight per thread; the one block
+// that straddles the buffer's end is read byte by byte by thread 0.
+__device__ __forceinline__ void stage_bytes(__amdgpu_buffer_rsrc_t r, uint32_t nbytes, uint32_t sb,
+                                            uint32_t sl, uint4 *dst) {
+  const uint32_t nch = sl >> 4;
+  const uint32_t nfull = nbytes > sb ? ((nbytes - sb) >> 4 < nch ? (nbytes - sb) >> 4 : nch) : 0u;
+  const int tid = threadIdx.x;
+  for (uint32_t i0 = 0; i0 < nfull; i0 += kSigThreads * 8) {
+    i32x4s v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint32_t i = i0 + u * kSigThreads + tid;
+      v[u] = i < nfull ? __builtin_amdgcn_raw_buffer_load_b128(r, (int)(sb + 16u * i), 0, 0)
+                       : i32x4s{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint32_t i = i0 + u * kSigThreads + tid;
+      if (i < nfull)
+        dst[i] = make_uint4((uint32_t)v[u][0], (uint32_t)v[u][1], (uint32_t)v[u][2],
+                            (uint32_t)v[u][3]);
+    }
+  }
+  if (tid == 0 && nfull < nch) {
+    uint32_t w[4];
+    load_window(r, sb + 16u * nfull, nbytes, w);
+    dst[nfull] = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+// The 16-byte window at `base` of a byte source: from the LDS copy when the
+// source was staged and the window lies inside it, else from global memory.
+__device__ __forceinline__ void fetch_window(bool staged, const uint4 *lds, uint32_t sb,
+                                             __amdgpu_buffer_rsrc_t r, uint32_t base,
+                                             uint32_t nbytes, uint32_t win[4]) {
+  if (staged) {
+    const uint4 x = lds[(base - sb) >> 4];
+    win[0] = x.x;
+    win[1] = x.y;
+    win[2] = x.z;
+    win[3] = x.w;
+  } else {
+    load_window(r, base, nbytes, win);
+  }
+}
+
+template <bool NORM>
 __global__ __launch_bounds__(kSigThreads) void signature_kernel(SigArgs a) {
   // all lanes read the same buffers: the descriptors are wave-uniform
   const __amdgpu_buffer_rsrc_t rp =
@@ -169,13 +223,42 @@ __global__ __launch_bounds__(kSigThreads) void signature_kernel(SigArgs a) {
   const uint32_t dig_bytes = (uint32_t)(a.first * 32);   // digests of earlier nodes only
   const __amdgpu_buffer_rsrc_t rd =
       __builtin_amdgcn_make_buffer_rsrc((void *)a.digest, (short)0, (int)dig_bytes, 0x00020000);
+  __shared__ uint4 s_text[kStageText / 16];
+  __shared__ uint4 s_par[kStageParam / 16];
+  __shared__ uint32_t s_msg[kMsgWords * kSigThreads];
+  const int64_t vend = a.first + a.count;
 
-  for (int64_t v = a.first + (int64_t)blockIdx.x * kSigThreads + threadIdx.x;
-       v < a.first + a.count; v += (int64_t)gridDim.x * kSigThreads) {
+  // Groups of kSigThreads consecutive nodes.  Their texts (and parameters)
+  // are consecutive in the buffers, so the group first copies the byte range
+  // from its first node's start to its last node's end into LDS (the first
+  // kStageText bytes of it); a thread whose text lies inside the copy reads
+  // it there, any other from global memory.
+  for (int64_t g0 = a.first + (int64_t)blockIdx.x * kSigThreads; g0 < vend;
+       g0 += (int64_t)gridDim.x * kSigThreads) {
+    const int64_t v = g0 + threadIdx.x;
+    const int64_t glast = (g0 + kSigThreads < vend ? g0 + kSigThreads : vend) - 1;
+    uint32_t gt0, gt1, gp0, gp1, dummy;
+    clamp_range(a.text_off, g0, a.text_bytes, gt0, dummy);
+    clamp_range(a.text_off, glast, a.text_bytes, dummy, gt1);
+    clamp_range(a.param_off, g0, a.param_bytes, gp0, dummy);
+    clamp_range(a.param_off, glast, a.param_bytes, dummy, gp1);
+    const uint32_t tsb = gt0 & ~15u, psb = gp0 & ~15u;
+    uint32_t tsl = gt1 > tsb ? ((gt1 - tsb + 15u) & ~15u) : 0u;
+    uint32_t psl = gp1 > psb ? ((gp1 - psb + 15u) & ~15u) : 0u;
+    tsl = tsl < kStageText ? tsl : kStageText;
+    psl = psl < kStageParam ? psl : kStageParam;
+    __syncthreads();   // the previous group is done with the copies
+    stage_bytes(rt, a.text_bytes, tsb, tsl, s_text);
+    stage_bytes(rp, a.param_bytes, psb, psl, s_par);
+    __syncthreads();
+    if (v >= vend) continue;
+
     const uint32_t tau = a.op_type[v];
     uint32_t p0, p1, t0, t1;
     clamp_range(a.param_off, v, a.param_bytes, p0, p1);
     clamp_range(a.text_off, v, a.text_bytes, t0, t1);
+    const bool t_lds = t0 >= tsb && t1 <= tsb + tsl;
+    const bool p_lds = p0 >= psb && p1 <= psb + psl;
     int64_t q0 = 0, q1 = 0;
     if (a.pred_off) {
       q0 = a.pred_off[v];
@@ -185,14 +268,111 @@ __global__ __launch_bounds__(kSigThreads) void signature_kernel(SigArgs a) {
     }
     const uint32_t P = p1 - p0, m = (uint32_t)(q1 - q0);
     uint32_t win[4];
+    uint32_t h[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[i] = kSha256H0[i];
+
+    if (16u + P + (t1 - t0) + 32u * m <= kMsgMax) {
+      // Short message: write it into this thread's LDS column (word j at
+      // s_msg[j * kSigThreads + tid], bytes in message order within a word),
+      // then compress its blocks.  The column layout keeps every LDS access
+      // of a wave on distinct banks.
+      uint8_t *col = (uint8_t *)s_msg;
+      const int tid = threadIdx.x;
+      auto put8 = [&](uint32_t o, uint32_t b) {
+        col[((o >> 2) * kSigThreads + tid) * 4 + (o & 3u)] = (uint8_t)b;
+      };
+      auto put32 = [&](uint32_t o, uint32_t x) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) put8(o + i, (x >> (8 * i)) & 0xffu);
+      };
+#pragma unroll
+      for (uint32_t j = 0; j < kMsgWords; ++j) s_msg[j * kSigThreads + tid] = 0u;
+      s_msg[tid] = tau;                    // le32(tau), bytes 0..3
+      s_msg[kSigThreads + tid] = P;        // le32(|Theta|), bytes 4..7
+      // Bytes are consumed one aligned 16-byte window at a time (every lane
+      // fetches its k-th window in the same iteration), with the window's
+      // bytes unrolled.  Each byte is written at the output position
+      // whether or not it is kept, and the position only advances past kept
+      // bytes, so a byte that is not kept is overwritten by the next one (or
+      // by the field that follows).
+      uint32_t o = 8u;
+      uint32_t gap = 0u;
+      for (uint32_t base = p0 & ~15u; base < p1; base += 16u) {
+        fetch_window(p_lds, s_par, psb, rp, base, a.param_bytes, win);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const uint32_t r = base + i;
+          put8(o, (win[i >> 2] >> (8 * (i & 3))) & 0xffu);
+          o += (uint32_t)(r >= p0) & (uint32_t)(r < p1);
+        }
+      }
+      const uint32_t o0 = 12u + P;         // first byte of D
+      o = o0;
+      for (uint32_t base = t0 & ~15u; base < t1; base += 16u) {
+        fetch_window(t_lds, s_text, tsb, rt, base, a.text_bytes, win);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const uint32_t r = base + i;
+          const uint32_t c = (win[i >> 2] >> (8 * (i & 3))) & 0xffu;
+          // (bitwise & and | on the flags: no short-circuit branches)
+          const uint32_t in = (uint32_t)(r >= t0) & (uint32_t)(r < t1);
+          if (!NORM) {
+            put8(o, c);
+            o += in;
+          } else {
+            const uint32_t sp = (uint32_t)(c == 0x20u) | (uint32_t)(c - 0x09u < 5u);
+            const uint32_t keep = in & (sp ^ 1u);
+            // a kept byte after a gap is preceded by one space, unless it
+            // is the first byte of D
+            put8(o, 0x20u);
+            o += keep & gap & (uint32_t)(o > o0);
+            put8(o, c + ((uint32_t)(c - 0x41u < 26u) << 5));
+            o += keep;
+            gap = (in & sp) | (gap & (in ^ 1u));
+          }
+        }
+      }
+      const uint32_t D = o - o0;
+      put32(8u + P, D);
+      put32(o, m);
+      o += 4;
+      for (uint32_t j = 0; j < m; ++j) {
+        const int64_t u = a.pred_idx[q0 + j];
+        uint32_t d8[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+        if (u >= 0 && u < a.first) {
+          load_window(rd, (uint32_t)u * 32u, dig_bytes, d8);
+          load_window(rd, (uint32_t)u * 32u + 16u, dig_bytes, d8 + 4);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) put32(o + 4 * i, d8[i]);
+        o += 32;
+      }
+      const uint32_t L = o;
+      const uint32_t nblk = (L + 8u) / 64u + 1u;
+      put8(L, 0x80u);
+      const uint64_t bits = (uint64_t)L * 8u;
+      // last 8 bytes: bit length, big-endian (the high three are zero)
+      const uint32_t e8 = nblk * 64u - 8u;
+#pragma unroll
+      for (int i = 3; i < 8; ++i) put8(e8 + i, (uint32_t)(bits >> (8 * (7 - i))) & 0xffu);
+      for (uint32_t bk = 0; bk < nblk; ++bk) {
+        uint32_t w[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          w[i] = __builtin_bswap32(s_msg[(bk * 16u + i) * kSigThreads + tid]);
+        sha256_block(h, w);
+      }
+    } else {
 
     // pass 1: length of D
     uint32_t D = t1 - t0;
-    if (a.normalize) {
+    if (NORM) {
       D = 0;
       bool gap = false;
       for (uint32_t r = t0; r < t1; ++r) {
-        if (r == t0 || (r & 15u) == 0) load_window(rt, r & ~15u, a.text_bytes, win);
+        if (r == t0 || (r & 15u) == 0)
+          fetch_window(t_lds, s_text, tsb, rt, r & ~15u, a.text_bytes, win);
         const uint32_t c = win_byte(win, r);
         if (ascii_space(c)) {
           gap = true;
@@ -209,26 +389,27 @@ __global__ __launch_bounds__(kSigThreads) void signature_kernel(SigArgs a) {
     const uint32_t end = nblk * 64u;
     const uint64_t bits = (uint64_t)L * 8u;
     const uint32_t sP = 8u, sDl = 8u + P, sD = 12u + P, sM = 12u + P + D, sQ = 16u + P + D;
-    uint32_t h[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) h[i] = kSha256H0[i];
     uint32_t w[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) w[i] = 0u;
-    uint32_t cur = 0u, nb = 0u, nw = 0u;
+    uint32_t cur = 0u;
     uint32_t rp_pos = p0, rt_pos = t0, wbase = 0xffffffffu;   // window state
     int src = -1;                                            // 0 params, 1 text, 2 digests
     bool gap = false;
     uint32_t emitted = 0u;
     int64_t pi = -1;   // current predecessor
-    for (uint32_t pos = 0; pos < end; ++pos) {
+    // Blocks in an outer loop, bytes in an inner one: the compression stays
+    // out of the byte loop, whose body is then only the byte source and the
+    // shift into the block's words.
+    for (uint32_t pos = 0; pos < end;) {
+     for (uint32_t i = 0; i < 64u; ++i, ++pos) {
       uint32_t b;
       if (pos < sP) {
         b = ((pos < 4u ? tau : P) >> ((pos & 3u) * 8u)) & 0xffu;
       } else if (pos < sDl) {
         if (src != 0 || (rp_pos & ~15u) != wbase) {
           wbase = rp_pos & ~15u;
-          load_window(rp, wbase, a.param_bytes, win);
+          fetch_window(p_lds, s_par, psb, rp, wbase, a.param_bytes, win);
           src = 0;
         }
         b = win_byte(win, rp_pos);
@@ -241,11 +422,11 @@ __global__ __launch_bounds__(kSigThreads) void signature_kernel(SigArgs a) {
         for (;;) {
           if (src != 1 || (rt_pos & ~15u) != wbase) {
             wbase = rt_pos & ~15u;
-            load_window(rt, wbase, a.text_bytes, win);
+            fetch_window(t_lds, s_text, tsb, rt, wbase, a.text_bytes, win);
             src = 1;
           }
           const uint32_t c = win_byte(win, rt_pos);
-          if (!a.normalize) {
+          if (!NORM) {
             b = c;
             ++rt_pos;
             break;
@@ -290,18 +471,16 @@ __global__ __launch_bounds__(kSigThreads) void signature_kernel(SigArgs a) {
         b = 0u;
       }
       cur = (cur << 8) | b;
-      if (++nb == 4u) {
+      if ((i & 3u) == 3u) {
 #pragma unroll
-        for (int i = 0; i < 15; ++i) w[i] = w[i + 1];
+        for (int j = 0; j < 15; ++j) w[j] = w[j + 1];
         w[15] = cur;
         cur = 0u;
-        nb = 0u;
-        if (++nw == 16u) {
-          sha256_block(h, w);
-          nw = 0u;
-        }
       }
+     }
+     sha256_block(h, w);
     }
+    }   // long message
 
     uint4 *dst = (uint4 *)(a.digest + v * 32);
     dst[0] = make_uint4(__builtin_bswap32(h[0]), __builtin_bswap32(h[1]),
@@ -337,7 +516,11 @@ hipError_t launch_signature(const uint32_t *op_type, const uint8_t *params,
   a.keys = keys;
   int64_t blocks = (count + kSigThreads - 1) / kSigThreads;
   if (blocks > 8192) blocks = 8192;
-  hipLaunchKernelGGL(signature_kernel, dim3((unsigned)blocks), dim3(kSigThreads), 0, st, a);
+  if (normalize)
+    hipLaunchKernelGGL(signature_kernel<true>, dim3((unsigned)blocks), dim3(kSigThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL(signature_kernel<false>, dim3((unsigned)blocks), dim3(kSigThreads), 0, st,
+                       a);
   return hipGetLastError();
 }
 

@@ -182,3 +182,17 @@ def test_whole_path_on_device_keys():
                                   ref["first_index"])
     check_unique_topk(m, ref, w.q_req, w.corpus, w.k)
     check_delivery(m, w.R)
+
+
+def test_group_text_beyond_the_lds_copy():
+    # 60 texts of ~2 KB in one group of nodes: the group's text range exceeds
+    # the bytes it copies to LDS, so later nodes read global memory
+    rng = np.random.default_rng(9)
+    alphabet = np.frombuffer(b"  \tAbcXyz\n", dtype=np.uint8)
+    texts = [bytes(alphabet[rng.integers(0, len(alphabet), size=int(rng.integers(1500, 2600)))])
+             for _ in range(60)]
+    t, toff = _pack(texts)
+    assert len(t) > 48 * 1024
+    op = np.full(60, 4, dtype=np.uint32)
+    _check(op, None, None, t, toff, None, None, [(0, 60)], True)
+    _check(op, None, None, t, toff, None, None, [(0, 60)], False)
