@@ -232,17 +232,17 @@ struct MfmaArgs {
 // stage is permuted identically for both operands: step t in 0..3 and lane
 // half h take elements [32h + 8t, 32h + 8t + 8), so that one 16-byte fp8
 // corpus piece feeds two consecutive steps.
-template <bool FP8>
+template <bool FP8, int NQB>
 struct Frag {
   // bf16: A pieces [step][rb]; fp8: raw 16-byte pieces [rb] (both steps)
   uint4 a[FP8 ? 1 : 2][kMRB];
-  uint4 b[2][kMQB];
+  uint4 b[2][NQB];
 };
 
 // Read half u of the stage in ring slot `st`.
-template <bool FP8>
-__device__ __forceinline__ void read_frags(Frag<FP8> &f, const unsigned char *st, int wv, int c,
-                                           int h, int u) {
+template <bool FP8, int NQB>
+__device__ __forceinline__ void read_frags(Frag<FP8, NQB> &f, const unsigned char *st, int wv,
+                                           int c, int h, int u) {
   using G = Geo<FP8>;
   const unsigned char *abase = st + (wv * 32 * kMRB + c) * G::arow;
   const unsigned char *bbase = st + G::abytes + c * G::brow;
@@ -264,7 +264,7 @@ __device__ __forceinline__ void read_frags(Frag<FP8> &f, const unsigned char *st
   for (int s = 0; s < 2; ++s) {
     const int slot = swz_slot<G::bpieces>(4 * h + 2 * u + s, c);
 #pragma unroll
-    for (int qb = 0; qb < kMQB; ++qb)
+    for (int qb = 0; qb < NQB; ++qb)
       f.b[s][qb] = *reinterpret_cast<const uint4 *>(bbase + qb * 32 * G::brow + slot * 16);
   }
 }
@@ -277,17 +277,17 @@ __device__ __forceinline__ void pin_u4(uint4 &v) {
   asm volatile("" : "+v"(t));
   v = __builtin_bit_cast(uint4, t);
 }
-template <bool FP8>
-__device__ __forceinline__ void pin_step1(Frag<FP8> &f) {
+template <bool FP8, int NQB>
+__device__ __forceinline__ void pin_step1(Frag<FP8, NQB> &f) {
 #pragma unroll
   for (int rb = 0; rb < kMRB; ++rb) pin_u4(f.a[FP8 ? 0 : 1][rb]);
 #pragma unroll
-  for (int qb = 0; qb < kMQB; ++qb) pin_u4(f.b[1][qb]);
+  for (int qb = 0; qb < NQB; ++qb) pin_u4(f.b[1][qb]);
 }
 
-// One 16-deep MFMA step over the wave's 4 x 4 blocks.
-template <bool FP8, bool ZERO>
-__device__ __forceinline__ void mfma_step(f32x16m (&acc)[kMRB][kMQB], const Frag<FP8> &f,
+// One 16-deep MFMA step over the wave's kMRB x NQB blocks.
+template <bool FP8, bool ZERO, int NQB>
+__device__ __forceinline__ void mfma_step(f32x16m (&acc)[kMRB][NQB], const Frag<FP8, NQB> &f,
                                           int s) {
   bf16x8m av[kMRB];
 #pragma unroll
@@ -304,7 +304,7 @@ __device__ __forceinline__ void mfma_step(f32x16m (&acc)[kMRB][kMQB], const Frag
 #pragma unroll
   for (int rb = 0; rb < kMRB; ++rb)
 #pragma unroll
-    for (int qb = 0; qb < kMQB; ++qb)
+    for (int qb = 0; qb < NQB; ++qb)
       acc[rb][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
           av[rb], __builtin_bit_cast(bf16x8m, f.b[s][qb]), ZERO ? zero : acc[rb][qb], 0, 0, 0);
 }
@@ -446,11 +446,12 @@ __device__ __forceinline__ void merge_queue(const MLds &L, const MfmaArgs &a, co
 // Keep the accumulators in AGPRs and make the compiler forget any VGPR copy
 // of them: the epilogue then reads each element where it is used instead of
 // holding all 256 in VGPRs across its loops.
-__device__ __forceinline__ void pin_acc(f32x16m (&acc)[kMRB][kMQB]) {
+template <int NQB>
+__device__ __forceinline__ void pin_acc(f32x16m (&acc)[kMRB][NQB]) {
 #pragma unroll
   for (int rb = 0; rb < kMRB; ++rb)
 #pragma unroll
-    for (int qb = 0; qb < kMQB; ++qb) asm volatile("" : "+a"(acc[rb][qb]));
+    for (int qb = 0; qb < NQB; ++qb) asm volatile("" : "+a"(acc[rb][qb]));
 }
 
 // An opaque copy of a lane value: values derived from it are recomputed
@@ -466,8 +467,8 @@ __device__ __forceinline__ int opaque(int x) {
 // rb * 32 + 8 * (i / 4) + i % 4 counted from the lane's first row; `lim0` =
 // number of valid rows from there.  Everything after reads the accumulators
 // directly.
-template <bool FP8>
-__device__ __forceinline__ void finish_scores(f32x16m (&acc)[kMRB][kMQB], const float *ssc_lane,
+template <bool FP8, int NQB>
+__device__ __forceinline__ void finish_scores(f32x16m (&acc)[kMRB][NQB], const float *ssc_lane,
                                               int lim0) {
   if constexpr (FP8) {
 #pragma unroll
@@ -478,7 +479,7 @@ __device__ __forceinline__ void finish_scores(f32x16m (&acc)[kMRB][kMQB], const 
         // ahead of the multiplies)
         const float4 s4 = *reinterpret_cast<const float4 *>(ssc_lane + opaque(rb * 32 + 8 * j));
 #pragma unroll
-        for (int qb = 0; qb < kMQB; ++qb) {
+        for (int qb = 0; qb < NQB; ++qb) {
           acc[rb][qb][4 * j + 0] *= s4.x;
           acc[rb][qb][4 * j + 1] *= s4.y;
           acc[rb][qb][4 * j + 2] *= s4.z;
@@ -492,7 +493,7 @@ __device__ __forceinline__ void finish_scores(f32x16m (&acc)[kMRB][kMQB], const 
 #pragma unroll
     for (int rb = 0; rb < kMRB; ++rb)
 #pragma unroll
-      for (int qb = 0; qb < kMQB; ++qb)
+      for (int qb = 0; qb < NQB; ++qb)
 #pragma unroll
         for (int i = 0; i < 16; ++i)
           if (rb * 32 + 8 * (i >> 2) + (i & 3) >= lim0) acc[rb][qb][i] = nan;
@@ -500,13 +501,14 @@ __device__ __forceinline__ void finish_scores(f32x16m (&acc)[kMRB][kMQB], const 
   }
 }
 // NaN for the scores of rows past N (only for a tile that reaches past N).
-__device__ __forceinline__ void mask_tail(f32x16m (&acc)[kMRB][kMQB], int lim0) {
+template <int NQB>
+__device__ __forceinline__ void mask_tail(f32x16m (&acc)[kMRB][NQB], int lim0) {
   if (lim0 < 32 * kMRB) {   // some of this lane's rows are past N
     const float nan = __builtin_nanf("");
 #pragma unroll
     for (int rb = 0; rb < kMRB; ++rb)
 #pragma unroll
-      for (int qb = 0; qb < kMQB; ++qb)
+      for (int qb = 0; qb < NQB; ++qb)
 #pragma unroll
         for (int i = 0; i < 16; ++i)
           if (rb * 32 + 8 * (i >> 2) + (i & 3) >= lim0) acc[rb][qb][i] = nan;
@@ -541,11 +543,11 @@ __device__ __forceinline__ void row_scales(float (&s16)[16], const float *ssc_la
 // Warm-up: per query, the smallest of this lane's group maxima (groups of
 // SPAN consecutive scores), combined over the two lane halves and stored per
 // wave.
-template <int SPAN>
-__device__ __forceinline__ void warm_minima(const MLds &L, f32x16m (&acc)[kMRB][kMQB], int wv,
+template <int SPAN, int NQB>
+__device__ __forceinline__ void warm_minima(const MLds &L, f32x16m (&acc)[kMRB][NQB], int wv,
                                             int c, int h) {
 #pragma unroll
-  for (int qb = 0; qb < kMQB; ++qb) {
+  for (int qb = 0; qb < NQB; ++qb) {
     float mn = __builtin_inff(), m = -__builtin_inff();
 #pragma unroll
     for (int rb = 0; rb < kMRB; ++rb)
@@ -567,9 +569,9 @@ __device__ __forceinline__ void warm_minima(const MLds &L, f32x16m (&acc)[kMRB][
 // are scores of distinct corpus rows, so the k-th largest of all of a
 // query's lane maxima (over all slices) is a lower bound of its k-th best
 // score over the whole corpus.
-template <bool FP8>
+template <bool FP8, int NQB>
 __device__ __forceinline__ void mtile_lane_maxima(const MfmaArgs &a, const MItem &it,
-                                                  f32x16m (&acc)[kMRB][kMQB], int row0,
+                                                  f32x16m (&acc)[kMRB][NQB], int row0,
                                                   const float *ssc) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int c = lane & 31, h = lane >> 5;
@@ -579,7 +581,7 @@ __device__ __forceinline__ void mtile_lane_maxima(const MfmaArgs &a, const MItem
   pin_acc(acc);
   finish_scores<FP8>(acc, ssc_lane, lim0);
 #pragma unroll
-  for (int qb = 0; qb < kMQB; ++qb) {
+  for (int qb = 0; qb < NQB; ++qb) {
     float m = -__builtin_inff();
 #pragma unroll
     for (int rb = 0; rb < kMRB; ++rb)
@@ -594,9 +596,9 @@ __device__ __forceinline__ void mtile_lane_maxima(const MfmaArgs &a, const MItem
 
 // Top-k epilogue of one tile.  row0 = corpus row of the tile's first row;
 // ssc = row scales of the tile (fp8).
-template <bool FP8, bool LDS_LISTS>
+template <bool FP8, bool LDS_LISTS, int NQB>
 __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a, const MItem &it,
-                                               f32x16m (&acc)[kMRB][kMQB],
+                                               f32x16m (&acc)[kMRB][NQB],
                                                float (&thr_r)[kMQB], int &epoch, int row0,
                                                const float *ssc, const uint32_t *gt,
                                                bool first) {
@@ -621,13 +623,13 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
     // queue, which these minima alias, is empty at an item's first tile)
     bar_lds();
     switch (gpl) {
-      case 1: warm_minima<kMVals / 1>(L, acc, wv, c, h); break;
-      case 2: warm_minima<kMVals / 2>(L, acc, wv, c, h); break;
-      case 4: warm_minima<kMVals / 4>(L, acc, wv, c, h); break;
-      case 8: warm_minima<kMVals / 8>(L, acc, wv, c, h); break;
-      case 16: warm_minima<kMVals / 16>(L, acc, wv, c, h); break;
-      case 32: warm_minima<kMVals / 32>(L, acc, wv, c, h); break;
-      default: warm_minima<1>(L, acc, wv, c, h); break;
+      case 1: warm_minima<kMVals / 1, NQB>(L, acc, wv, c, h); break;
+      case 2: warm_minima<kMVals / 2, NQB>(L, acc, wv, c, h); break;
+      case 4: warm_minima<kMVals / 4, NQB>(L, acc, wv, c, h); break;
+      case 8: warm_minima<kMVals / 8, NQB>(L, acc, wv, c, h); break;
+      case 16: warm_minima<kMVals / 16, NQB>(L, acc, wv, c, h); break;
+      case 32: warm_minima<kMVals / 32, NQB>(L, acc, wv, c, h); break;
+      default: warm_minima<1, NQB>(L, acc, wv, c, h); break;
     }
     bar_lds();
     if (tid < it.qvalid) {
@@ -656,15 +658,15 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
   // as still to be examined; a 16-score row block is eligible when its best
   // score reaches the query threshold.
   pin_acc(acc);
-  uint64_t elig[kMQB];
+  uint64_t elig[NQB];
 #pragma unroll
-  for (int qb = 0; qb < kMQB; ++qb) elig[qb] = 0ull;
+  for (int qb = 0; qb < NQB; ++qb) elig[qb] = 0ull;
 #pragma unroll
   for (int rb = 0; rb < kMRB; ++rb) {
     float s16[16];
     row_scales<FP8>(s16, ssc_lane, rb, scaled);
 #pragma unroll
-    for (int qb = 0; qb < kMQB; ++qb) {
+    for (int qb = 0; qb < NQB; ++qb) {
       float m = ninf;
 #pragma unroll
       for (int i = 0; i < 16; ++i) m = fmaxf(m, FP8 ? acc[rb][qb][i] * s16[i] : acc[rb][qb][i]);
@@ -672,7 +674,7 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
     }
   }
 #pragma unroll
-  for (int qb = 0; qb < kMQB; ++qb)
+  for (int qb = 0; qb < NQB; ++qb)
     if (qb * 32 + c >= it.qvalid) elig[qb] = 0ull;
   // Scores at or above the current threshold are appended to the per-query
   // LDS queues (atomics, no barrier).  Merges into the k-lists are deferred:
@@ -684,7 +686,7 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
     bool ovf = false, full = false;
     pin_acc(acc);
 #pragma unroll
-    for (int qb = 0; qb < kMQB; ++qb) {
+    for (int qb = 0; qb < NQB; ++qb) {
       const int ql = qb * 32 + c;
       const float th = thr_r[qb];
       uint64_t fail = 0;
@@ -752,27 +754,23 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
   }
 }
 
-template <bool FP8, bool LDS_LISTS, bool SEED>
-__global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
+// One work item (a query tile against one corpus slice) whose queries fill
+// NQB of the tile's 32-query blocks: the fragment reads, the matrix-core
+// steps and the epilogue skip the blocks past the item's queries (a partial
+// last query tile, or few distinct queries).  The copies are those of a full
+// tile (the query rows past the item's queries read as zeros).
+template <bool FP8, bool LDS_LISTS, bool SEED, int NQB>
+__device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const Split &sp,
+                                         int64_t nu, int w, int &epoch) {
   using G = Geo<FP8>;
-  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
-  const MLds L = carve_mlds<FP8, LDS_LISTS>(smem, a.k);
-
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int c = lane & 31, h = lane >> 5;
-  const int64_t nu = read_nu(a.n_unique, a.n_unique_dev, a.cap);
-  int64_t smax = kMSplitMaxSK / a.k;
-  const Split sp = make_split(nu, a.N, kMMQ, kMNC, a.grid, smax < 1 ? 1 : smax);
-  const int items = (int)(sp.qtiles * sp.S);
   const int N = (int)a.N, d = (int)a.d;
   const int nch = (d + kMKC - 1) / kMKC;
   const float ninf = -__builtin_inff();
-  if (tid < 4) L.flags[tid] = 0;
-  int epoch = 1;
-
   // (the per-lane copy offsets are recomputed at each copy from the lane id,
   // a few VALU operations, rather than held in registers across the loop)
-  for (int w = logical_wg(a.grid); w < items; w += a.grid) {
+  {
     MItem it;
     const int qt = w % (int)sp.qtiles;
     it.s = w / (int)sp.qtiles;
@@ -899,8 +897,8 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
 
 #pragma unroll
     for (int qb = 0; qb < kMQB; ++qb) thr_r[qb] = L.thr[qb * 32 + c];
-    f32x16m acc[kMRB][kMQB];
-    Frag<FP8> f0, f1;
+    f32x16m acc[kMRB][NQB];
+    Frag<FP8, NQB> f0, f1;
     read_frags<FP8>(f0, L.ring, wv, c, h, 0);
     int r_slot = 0, e_sc = 0, e_gt = 0, g = 0;
 
@@ -981,6 +979,30 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
     }
     wait_vm(0);
     bar_lds();
+  }
+}
+
+template <bool FP8, bool LDS_LISTS, bool SEED>
+__global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
+  const MLds L = carve_mlds<FP8, LDS_LISTS>(smem, a.k);
+  const int64_t nu = read_nu(a.n_unique, a.n_unique_dev, a.cap);
+  int64_t smax = kMSplitMaxSK / a.k;
+  const Split sp = make_split(nu, a.N, kMMQ, kMNC, a.grid, smax < 1 ? 1 : smax);
+  const int items = (int)(sp.qtiles * sp.S);
+  if (threadIdx.x < 4) L.flags[threadIdx.x] = 0;
+  int epoch = 1;
+  for (int w = logical_wg(a.grid); w < items; w += a.grid) {
+    // queries of the item's tile (at least one: the tiles cover n_u)
+    const int64_t qv = nu - (int64_t)(w % (int)sp.qtiles) * kMMQ;
+    if (qv > 96)
+      run_item<FP8, LDS_LISTS, SEED, 4>(a, L, sp, nu, w, epoch);
+    else if (qv > 64)
+      run_item<FP8, LDS_LISTS, SEED, 3>(a, L, sp, nu, w, epoch);
+    else if (qv > 32)
+      run_item<FP8, LDS_LISTS, SEED, 2>(a, L, sp, nu, w, epoch);
+    else
+      run_item<FP8, LDS_LISTS, SEED, 1>(a, L, sp, nu, w, epoch);
   }
 }
 
