@@ -756,8 +756,8 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
 
 // One work item (a query tile against one corpus slice) whose queries fill
 // NQB of the tile's 32-query blocks: the fragment reads, the matrix-core
-// steps and the epilogue skip the blocks past the item's queries (a partial
-// last query tile, or few distinct queries).  The copies are those of a full
+// steps and the epilogue skip the blocks past the item's queries (few
+// distinct queries).  The copies are those of a full
 // tile (the query rows past the item's queries read as zeros).
 template <bool FP8, bool LDS_LISTS, bool SEED, int NQB>
 __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const Split &sp,
@@ -993,8 +993,12 @@ __global__ __launch_bounds__(kMT, 1) void score_mfma_dma(MfmaArgs a) {
   if (threadIdx.x < 4) L.flags[threadIdx.x] = 0;
   int epoch = 1;
   for (int w = logical_wg(a.grid); w < items; w += a.grid) {
-    // queries of the item's tile (at least one: the tiles cover n_u)
-    const int64_t qv = nu - (int64_t)(w % (int)sp.qtiles) * kMMQ;
+    // Queries of the item's tile (at least one: the tiles cover n_u).  With
+    // several query tiles, the items of one corpus slice run on neighbouring
+    // workgroups of one XCD and share its L2 only while they run at the same
+    // pace, so every item then runs as a full tile; a single (partial) tile
+    // skips its empty query blocks.
+    const int64_t qv = sp.qtiles > 1 ? kMMQ : nu;
     if (qv > 96)
       run_item<FP8, LDS_LISTS, SEED, 4>(a, L, sp, nu, w, epoch);
     else if (qv > 64)
