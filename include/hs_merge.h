@@ -89,7 +89,8 @@ typedef struct hs_plan hs_plan;   /* opaque, immutable, thread-safe host object 
 
 /* Validate `desc` and create a plan.  *workspace_bytes receives the size of the
  * device workspace that hs_dedup and hs_score_topk (and its two phases) need
- * for this shape.  The plan is freed with hs_plan_destroy. */
+ * for this shape (it also covers hs_priority).  The plan is freed with
+ * hs_plan_destroy. */
 hs_status hs_merge_plan(const hs_merge_desc *desc, hs_plan **plan, size_t *workspace_bytes);
 
 void hs_plan_destroy(hs_plan *plan);
@@ -259,6 +260,34 @@ typedef struct {
  * 32 zero bytes.  Bit-exact and deterministic. */
 hs_status hs_signature(const hs_sig_nodes *nodes, int64_t first, int64_t count, int32_t flags,
                        uint8_t *digest, int64_t *keys, void *stream);
+
+/* Reuse-driven priorities of the fused nodes (Eq. 3) and their order in the
+ * ready queue (Eq. 7; Algorithm 1, phase 2), from hs_dedup's groups:
+ *   inverse, first_index  hs_dedup outputs ([R] and [n_u] int32 device)
+ *   n_unique / n_unique_dev  as for hs_score_topk
+ *   phi      [R] fp32 device: contribution phi_v of each logical node (Eq. 5,
+ *            computed upstream); clamped to [0, 2^16), NaN counts as 0
+ *   s_hat    [R] fp32 device: remaining-time estimate S_q of each node's
+ *            query (Eq. 4, computed upstream), >= 0
+ *   heavy    [R] uint8 device, may be NULL (all 0): heavy-node flag y_v
+ *   alpha, gamma, delta, eps  the weights of Eq. 7 (finite; eps > 0)
+ *   phi_fused [n_u] fp64 device out, may be NULL: phi* of Eq. 3 = the sum of
+ *            the group's phi_v, each truncated to a multiple of 2^-24 first;
+ *            exact (independent of the order of the additions) and rounded
+ *            once to fp64, for groups whose sum stays below 2^39
+ *   pi       [n_u] fp64 device out, may be NULL:
+ *            ((alpha / (s_hat[s] + eps)) + gamma * phi*) + delta * heavy[s],
+ *            each operation rounded to nearest, s = first_index[g] (the
+ *            surviving node, to which the merged nodes' edges are redirected)
+ *   order    [n_u] int32 device out: the fused nodes by pi descending, equal
+ *            pi by ascending group (-0 as +0)
+ *   ws       the plan's workspace (hs_merge_plan's size covers this call)
+ * Bit-exact and deterministic. */
+hs_status hs_priority(const hs_plan *plan, const int32_t *inverse, const int32_t *first_index,
+                      int64_t n_unique, const int64_t *n_unique_dev, const float *phi,
+                      const float *s_hat, const uint8_t *heavy, double alpha, double gamma,
+                      double delta, double eps, double *phi_fused, double *pi, int32_t *order,
+                      void *ws, size_t ws_bytes, void *stream);
 
 const char *hs_status_string(hs_status s);
 const char *hs_last_error(void);

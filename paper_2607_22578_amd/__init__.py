@@ -37,8 +37,8 @@ ABI_VERSION = 1
 
 EXPORTS = ["hs_merge_plan", "hs_plan_destroy", "hs_dedup", "hs_score_topk", "hs_score_partial",
            "hs_topk_merge", "hs_scatter", "hs_cache_bytes", "hs_cache_reset", "hs_cache_lookup",
-           "hs_cache_insert", "hs_signature", "hs_status_string", "hs_last_error",
-           "hs_abi_version"]
+           "hs_cache_insert", "hs_signature", "hs_priority", "hs_status_string",
+           "hs_last_error", "hs_abi_version"]
 HS_SIG_NORMALIZE_TEXT = 1
 
 
@@ -84,6 +84,10 @@ _lib.hs_cache_insert.argtypes = [_vp, _vp, _sz, _i64, _vp, _vp, _i64, _vp, _vp, 
 _lib.hs_cache_insert.restype = ctypes.c_int
 _lib.hs_signature.argtypes = [ctypes.POINTER(hs_sig_nodes), _i64, _i64, _i32, _vp, _vp, _vp]
 _lib.hs_signature.restype = ctypes.c_int
+_dbl = ctypes.c_double
+_lib.hs_priority.argtypes = ([_vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _dbl, _dbl, _dbl, _dbl]
+                             + [_vp] * 4 + [_sz, _vp])
+_lib.hs_priority.restype = ctypes.c_int
 _lib.hs_status_string.argtypes = [ctypes.c_int]
 _lib.hs_status_string.restype = ctypes.c_char_p
 _lib.hs_last_error.argtypes = []
@@ -264,6 +268,15 @@ def hs_signature(op_type, n_nodes: int, first: int, count: int, digest, keys=Non
                              _stream(stream)))
 
 
+def hs_priority(plan: Plan, inverse, first_index, n_unique: int, n_unique_dev, phi, s_hat, heavy,
+                alpha: float, gamma: float, delta: float, eps: float, phi_fused, pi, order,
+                ws=None, ws_bytes: Optional[int] = None, stream=None):
+    _check(_lib.hs_priority(plan.handle, _ptr(inverse), _ptr(first_index), n_unique,
+                            _ptr(n_unique_dev), _ptr(phi), _ptr(s_hat), _ptr(heavy), alpha, gamma,
+                            delta, eps, _ptr(phi_fused), _ptr(pi), _ptr(order), _ptr(ws),
+                            _ws_bytes(ws, ws_bytes), _stream(stream)))
+
+
 # ---------------------------------------------------------------- composition
 
 class MergedRetrieval:
@@ -376,3 +389,22 @@ class MergedRetrieval:
                         self.miss_pos, -1, self.n_unique, self.topk_score, self.topk_index,
                         stream=stream)
         self.deliver(stream)
+
+    # ------------------------------------------------ ready-queue priorities
+
+    def priority(self, phi, s_hat, heavy=None, alpha=1.0, gamma=1.0, delta=0.0, eps=1e-6,
+                 stream=None):
+        """Eq. 3 / Eq. 7 priorities of this window's fused nodes (after dedup)
+        and their ready-queue order; results in self.phi_fused, self.pi,
+        self.order (first n_u entries)."""
+        import torch
+        dev = self.ws.device
+        if not hasattr(self, "order"):
+            c1 = max(self.cap, 1)
+            self.phi_fused = torch.empty(c1, dtype=torch.float64, device=dev)
+            self.pi = torch.empty(c1, dtype=torch.float64, device=dev)
+            self.order = torch.empty(c1, dtype=torch.int32, device=dev)
+        hs_priority(self.plan, self.inverse, self.first_index, -1, self.n_unique, phi, s_hat,
+                    heavy, alpha, gamma, delta, eps, self.phi_fused, self.pi, self.order, self.ws,
+                    stream=stream)
+

@@ -6,6 +6,7 @@
 // touched.  No entry point allocates device memory.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -43,6 +44,12 @@ hipError_t launch_signature(const uint32_t *op_type, const uint8_t *params,
                             const int32_t *pred_idx, int64_t pred_count, int64_t first,
                             int64_t count, int normalize, uint8_t *digest, int64_t *keys,
                             hipStream_t st);
+size_t priority_workspace_bytes(int64_t cap);
+hipError_t launch_priority(const int32_t *inverse, const int32_t *first_index, int64_t R,
+                           int64_t n_unique, const int64_t *nu_dev, int64_t cap,
+                           const float *phi, const float *s_hat, const uint8_t *heavy,
+                           double alpha, double gamma, double delta, double eps, double *phi_out,
+                           double *pi_out, int32_t *order, void *ws, hipStream_t st);
 }  // namespace hs
 
 struct hs_plan {
@@ -50,6 +57,7 @@ struct hs_plan {
   int64_t cap;          // max distinct keys
   size_t ws_dedup;      // bytes used by hs_dedup (offset 0)
   size_t ws_score;      // bytes used by the score phases (offset 0)
+  size_t ws_prio;       // bytes used by hs_priority (offset 0)
   size_t ws_total;
 };
 
@@ -131,7 +139,9 @@ hs_status hs_merge_plan(const hs_merge_desc *desc, hs_plan **plan, size_t *works
   p->cap = d.max_unique > 0 ? d.max_unique : d.n_requests;
   p->ws_dedup = hs::dedup_workspace_bytes(d.n_requests);
   p->ws_score = hs::score_workspace_bytes(p->cap, d.n_corpus, d.k, d.corpus_dtype);
+  p->ws_prio = hs::priority_workspace_bytes(p->cap);
   p->ws_total = p->ws_dedup > p->ws_score ? p->ws_dedup : p->ws_score;
+  if (p->ws_prio > p->ws_total) p->ws_total = p->ws_prio;
   *plan = p;
   *workspace_bytes = p->ws_total;
   return ok();
@@ -392,6 +402,35 @@ hs_status hs_signature(const hs_sig_nodes *nd, int64_t first, int64_t count, int
       nd->pred_idx ? nd->pred_count : 0, first, count, (flags & HS_SIG_NORMALIZE_TEXT) ? 1 : 0,
       digest, keys, (hipStream_t)stream);
   return device_status(e, "hs_signature launch");
+}
+
+// ---------------------------------------------------------------- priorities
+
+hs_status hs_priority(const hs_plan *plan, const int32_t *inverse, const int32_t *first_index,
+                      int64_t n_unique, const int64_t *n_unique_dev, const float *phi,
+                      const float *s_hat, const uint8_t *heavy, double alpha, double gamma,
+                      double delta, double eps, double *phi_fused, double *pi, int32_t *order,
+                      void *ws, size_t ws_bytes, void *stream) {
+  if (!plan) return fail(HS_ERR_INVALID_ARG, "hs_priority: null plan");
+  hs_status s = check_nu(plan, n_unique, n_unique_dev, "hs_priority");
+  if (s != HS_OK) return s;
+  if (!std::isfinite(alpha) || !std::isfinite(gamma) || !std::isfinite(delta) ||
+      !std::isfinite(eps) || !(eps > 0.0))
+    return fail(HS_ERR_INVALID_ARG, "hs_priority: alpha, gamma, delta must be finite and eps > 0");
+  if (n_unique == 0) return ok();
+  if (!inverse || !first_index || !phi || !s_hat || !order)
+    return fail(HS_ERR_INVALID_ARG, "hs_priority: null argument");
+  if (!ws || ws_bytes < plan->ws_prio)
+    return fail(HS_ERR_WORKSPACE, "hs_priority: workspace has %zu bytes, needs %zu", ws_bytes,
+                plan->ws_prio);
+  if (!aligned(ws, 256)) return fail(HS_ERR_ALIGNMENT, "hs_priority: workspace not 256-aligned");
+  if (!aligned(inverse, 4) || !aligned(first_index, 4) || !aligned(phi, 4) ||
+      !aligned(s_hat, 4) || !aligned(order, 4) || !aligned(phi_fused, 8) || !aligned(pi, 8))
+    return fail(HS_ERR_ALIGNMENT, "hs_priority: misaligned pointer");
+  hipError_t e = hs::launch_priority(inverse, first_index, plan->d.n_requests, n_unique,
+                                     n_unique_dev, plan->cap, phi, s_hat, heavy, alpha, gamma,
+                                     delta, eps, phi_fused, pi, order, ws, (hipStream_t)stream);
+  return device_status(e, "hs_priority launch");
 }
 
 }  // extern "C"

@@ -32,6 +32,7 @@ _lib = None
 # named streams
 S_QUERY, S_CORPUS, S_TABLE, S_ZIPF, S_PERM, S_KEY, S_SLOTS = 1, 2, 3, 4, 5, 6, 7
 S_TEXT, S_RENDER = 8, 9
+S_SCHED = 10
 ENC = {"f32": 0, "bf16": 1, "fp8": 2}
 BASE_SEED = 20260722
 
@@ -340,4 +341,22 @@ def render_texts(seed: int, template_ids: np.ndarray, vary: bool = True):
     off[1:] = np.cumsum([len(x) for x in parts])
     buf = np.frombuffer(b"".join(parts), dtype=np.uint8).copy()
     return buf, off
+
+
+def scheduler_inputs(w: Workload):
+    """Per-request scheduler state for the priority step: phi (fp32, a mix of
+    a few repeated values -- so that fused sums tie -- and continuous values
+    in [0, 50)), the remaining-time estimate of each request's workflow
+    (fp32 in [0.1, 20), shared by the workflow's requests) and a heavy flag
+    per workflow (about 15 % of workflows)."""
+    g = np.random.default_rng([w.seed, S_SCHED])
+    R = w.R
+    n_wf = len(w.workflow_offsets) - 1
+    wf = np.repeat(np.arange(n_wf), np.diff(w.workflow_offsets))
+    discrete = np.array([0.5, 1.0, 2.0, 4.0], dtype=np.float32)[g.integers(0, 4, size=R)]
+    cont = (g.random(R) * 50).astype(np.float32)
+    phi = np.where(g.random(R) < 0.5, discrete, cont).astype(np.float32)
+    s_wf = (0.1 + g.random(n_wf) * 19.9).astype(np.float32)
+    heavy_wf = (g.random(n_wf) < 0.15).astype(np.uint8)
+    return phi, s_wf[wf], heavy_wf[wf]
 

@@ -191,3 +191,26 @@ def test_signature_validation():
             call(**bad)
         assert e.value.status == hs.HS_ERR_ALIGNMENT, bad
     call(count=0, first=10)   # empty range: nothing is enqueued
+
+
+def test_priority_validation():
+    p = hs.hs_merge_plan(**GOOD)
+    ws = p.workspace_bytes
+    args = [FAKE, FAKE, 10, None, FAKE, FAKE, None, 1.0, 1.0, 0.0, 1e-3, FAKE, FAKE, FAKE, FAKE]
+    hs.hs_priority(p, *args[:2], 0, None, *args[4:], ws_bytes=ws)   # n_u = 0: no-op
+    for i, bad, code in [(2, 4096, hs.HS_ERR_INVALID_ARG),          # beyond the plan
+                         (2, -1, hs.HS_ERR_INVALID_ARG),            # -1 without device count
+                         (10, 0.0, hs.HS_ERR_INVALID_ARG),          # eps must be > 0
+                         (7, float("nan"), hs.HS_ERR_INVALID_ARG),  # alpha finite
+                         (0, None, hs.HS_ERR_INVALID_ARG),
+                         (13, None, hs.HS_ERR_INVALID_ARG),         # order
+                         (11, FAKE + 4, hs.HS_ERR_ALIGNMENT),       # fp64 output
+                         (14, FAKE + 64, hs.HS_ERR_ALIGNMENT)]:     # workspace
+        a = list(args)
+        a[i] = bad
+        with pytest.raises(hs.HsError) as e:
+            hs.hs_priority(p, *a, ws_bytes=ws)
+        assert e.value.status == code, (i, bad)
+    with pytest.raises(hs.HsError) as e:
+        hs.hs_priority(p, *args, ws_bytes=16)
+    assert e.value.status == hs.HS_ERR_WORKSPACE
