@@ -83,6 +83,12 @@ def parse():
     ap.add_argument("--sig-nodes", type=int, default=0,
                     help="only time hs_signature on this many request nodes of the workload's "
                          "traffic (one JSON line of its own)")
+    ap.add_argument("--priorities", action="store_true",
+                    help="each step also computes the fused nodes' priorities and ready-queue "
+                         "order (hs_priority) after the dedup")
+    ap.add_argument("--prio-only", default="",
+                    help="only time hs_dedup + hs_priority on this workload's requests (e.g. "
+                         "dedup256k; one JSON line of its own)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
     return ap.parse_args()
@@ -110,6 +116,9 @@ def main():
         return
     if args.sig_nodes:
         signature_bench(args)
+        return
+    if args.prio_only:
+        priority_bench(args)
         return
 
     import numpy as np
@@ -148,6 +157,11 @@ def main():
         sig = SigInputs(hs, dev, buf, off, k)
         keys = sig.keys
     sig_ev = {}
+    prio = None
+    if args.priorities:
+        phi_h, s_h, y_h = synth.scheduler_inputs(w)
+        prio = (to_dev(phi_h), to_dev(s_h), to_dev(y_h))
+    prio_ev = {}
     windows = None
     if args.reuse_store:
         # successive windows of the same traffic: window i is step i of the run
@@ -169,6 +183,12 @@ def main():
             m.run_cached(wk, wq, corpus, scale, stream, score_events=ev)
             return
         m.dedup(keys, stream)
+        if prio is not None:
+            if ev is not None:
+                prio_ev[id(ev)][0].record(stream)
+            m.priority(*prio, **PRIO_WEIGHTS, stream=stream)
+            if ev is not None:
+                prio_ev[id(ev)][1].record(stream)
         m.gather_queries(q_req, stream)
         if ev is not None:
             ev[0].record(stream)
@@ -192,6 +212,8 @@ def main():
     for e in evs.values():
         sig_ev[id(e)] = (torch.cuda.Event(enable_timing=True),
                          torch.cuda.Event(enable_timing=True))
+        prio_ev[id(e)] = (torch.cuda.Event(enable_timing=True),
+                          torch.cuda.Event(enable_timing=True))
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize(dev)
@@ -251,6 +273,12 @@ def main():
         sig_ms = float(np.mean([sig_ev[id(e)][0].elapsed_time(sig_ev[id(e)][1])
                                 for e in evs.values()]))
         sig_stats = sig.stats(sig_ms)
+    prio_stats = None
+    if prio is not None:
+        pms = float(np.mean([prio_ev[id(e)][0].elapsed_time(prio_ev[id(e)][1])
+                             for e in evs.values()]))
+        prio_stats = {"kernels": "priority_clear/sum/pi/chunk_sort/merge/order",
+                      "n_requests": R, "n_unique": n_u, "ms": round(pms, 4)}
     stages = dict(zip(["dedup", "gather", "score_partial", "topk_merge", "deliver"],
                       (acc / max(reps, 1)).round(4).tolist())) if reps else None
 
@@ -299,7 +327,7 @@ def main():
                    "dim": d, "n_corpus": N, "k": k, "query_dtype": cfg.q_enc,
                    "corpus_dtype": cfg.c_enc, "seed": w.seed,
                    "merge": not args.no_merge, "reuse": reuse,
-                   "signatures": args.signatures},
+                   "signatures": args.signatures, "priorities": args.priorities},
         "unique_queries_per_s": round(n_distinct * args.steps / (total_ms * 1e-3), 1),
         "stages_ms": stages,
         "wall_s_timed": round(wall, 4),
@@ -307,6 +335,8 @@ def main():
     }
     if sig_stats is not None:
         out["signature_step"] = sig_stats
+    if prio_stats is not None:
+        out["priority_step"] = prio_stats
 
     if not args.no_cpu_baseline and windows is None:
         out["cpu_baseline"] = cpu_baseline(w, n_u, args.cpu_sample)
@@ -404,6 +434,63 @@ def signature_bench(args):
                                   f"(Zipf({cfg.zipf_s}) over {cfg.n_templates} templates), "
                                   "normalised query text + Top-K parameter"},
            "roofline": st["roofline"], "signature_step": st}
+    print(json.dumps(out), flush=True)
+
+
+# weights of the priority function used by the priority modes
+PRIO_WEIGHTS = dict(alpha=2.0, gamma=0.75, delta=5.0, eps=0.25)
+
+
+def priority_bench(args):
+    """hs_dedup + hs_priority alone on one workload's requests."""
+    import numpy as np
+    import torch
+
+    import paper_2607_22578_amd as hs
+    import synth
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.make(args.prio_only, with_corpus=False)
+    phi, s_hat, heavy = synth.scheduler_inputs(w)
+    R = w.R
+    plan = hs.hs_merge_plan(R, 8, 1, 1, hs.HS_BF16, hs.HS_BF16)
+    ws = torch.empty(max(plan.workspace_bytes, 256), dtype=torch.uint8, device=dev)
+    kd = torch.from_numpy(w.keys).to(dev)
+    uk = torch.empty(R, dtype=torch.int64, device=dev)
+    fi = torch.empty(R, dtype=torch.int32, device=dev)
+    ct = torch.empty(R, dtype=torch.int32, device=dev)
+    inv = torch.empty(R, dtype=torch.int32, device=dev)
+    nu = torch.zeros(1, dtype=torch.int64, device=dev)
+    phf = torch.empty(R, dtype=torch.float64, device=dev)
+    pi = torch.empty(R, dtype=torch.float64, device=dev)
+    order = torch.empty(R, dtype=torch.int32, device=dev)
+    ph, sh, hv = (torch.from_numpy(x).to(dev) for x in (phi, s_hat, heavy))
+    stream = torch.cuda.Stream(dev)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    d_ms, p_ms = [], []
+    for i in range(args.warmup + args.steps):
+        evs[0].record(stream)
+        hs.hs_dedup(plan, kd, uk, fi, ct, inv, nu, None, ws, stream=stream)
+        evs[1].record(stream)
+        hs.hs_priority(plan, inv, fi, -1, nu, ph, sh, hv, PRIO_WEIGHTS["alpha"],
+                       PRIO_WEIGHTS["gamma"], PRIO_WEIGHTS["delta"], PRIO_WEIGHTS["eps"], phf,
+                       pi, order, ws, stream=stream)
+        evs[2].record(stream)
+        torch.cuda.synchronize(dev)
+        if i >= args.warmup:
+            d_ms.append(evs[0].elapsed_time(evs[1]))
+            p_ms.append(evs[1].elapsed_time(evs[2]))
+    n_u = int(nu.item())
+    tot = float(np.mean(d_ms)) + float(np.mean(p_ms))
+    out = {"metric": "fused-node priorities: requests/s through dedup + priority + order",
+           "value": round(R / (tot * 1e-3), 1), "unit": "requests/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(tot, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+           "data": "synthetic",
+           "config": {"workload": f"{w.cfg.name}: {w.cfg.desc}", "n_requests": R,
+                      "n_unique": n_u, "weights": PRIO_WEIGHTS},
+           "dedup_ms": round(float(np.mean(d_ms)), 4),
+           "priority_ms": round(float(np.mean(p_ms)), 4)}
     print(json.dumps(out), flush=True)
 
 

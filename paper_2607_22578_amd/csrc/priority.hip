@@ -46,30 +46,153 @@ __device__ __forceinline__ bool item_less(const SortItem &a, const SortItem &b) 
   return a.key < b.key || (a.key == b.key && a.g < b.g);
 }
 
+// phi_i in units of 2^-24 (clamped to [0, 2^16), NaN as 0; < 2^40)
+__device__ __forceinline__ uint64_t phi_units(float f) {
+  f = f > 0.0f ? f : 0.0f;                         // negative and NaN -> 0
+  f = f < 65536.0f ? f : 65535.99609375f;          // largest fp32 below 2^16
+  // f * 2^24 is exact in fp32; truncation gives the units
+  return (uint64_t)__float2ll_rz(f * 16777216.0f);
+}
+
+// phi* and pi of fused node g from its unit sum, and its sort item.
+__device__ __forceinline__ SortItem node_priority(uint64_t units, int64_t g,
+                                                  const int32_t *__restrict__ first_index,
+                                                  const float *__restrict__ s_hat,
+                                                  const uint8_t *__restrict__ heavy, int64_t R,
+                                                  double alpha, double gamma, double delta,
+                                                  double eps, double *__restrict__ phi_out,
+                                                  double *__restrict__ pi_out) {
+  // units < 2^63: one correctly rounded conversion, then an exact scaling
+  const double ph = __dmul_rn(__ll2double_rn((long long)units), 1.0 / kPhiUnit);
+  const int64_t s = first_index[g];
+  const bool ok = s >= 0 && s < R;
+  const double sq = ok ? (double)s_hat[s] : 0.0;
+  const double y = ok && heavy ? (heavy[s] ? 1.0 : 0.0) : 0.0;
+  double p = __dadd_rn(__ddiv_rn(alpha, __dadd_rn(sq, eps)), __dmul_rn(gamma, ph));
+  p = __dadd_rn(p, __dmul_rn(delta, y));
+  p = p == 0.0 ? 0.0 : p;   // -0 -> +0
+  if (phi_out) phi_out[g] = ph;
+  if (pi_out) pi_out[g] = p;
+  const uint64_t b = (uint64_t)__double_as_longlong(p);
+  const uint64_t ord = (b >> 63) ? ~b : (b | 0x8000000000000000ull);   // ascending with pi
+  SortItem it;
+  it.key = ~ord;
+  it.g = (uint32_t)g;
+  it.pad = 0u;
+  return it;
+}
+
+// In-place ascending bitonic sort of sh[0, p2) (p2 a power of two, padded).
+__device__ __forceinline__ void bitonic_lds(SortItem *sh, int p2) {
+  const int tid = threadIdx.x;
+  for (int size = 2; size <= p2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid; i < p2 / 2; i += blockDim.x) {
+        const int lo = 2 * i - (i & (stride - 1));
+        const int hi = lo + stride;
+        const bool up = (lo & size) == 0;
+        const SortItem a = sh[lo], b = sh[hi];
+        if (item_less(b, a) == up) {
+          sh[lo] = b;
+          sh[hi] = a;
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+__device__ __forceinline__ SortItem pad_item() {
+  SortItem pad;
+  pad.key = ~0ull;
+  pad.g = 0xffffffffu;
+  pad.pad = 0u;
+  return pad;
+}
+
+// The whole step in one workgroup when at most kSortChunk fused nodes are
+// possible: unit sums in LDS (64-bit LDS atomics), priorities, sort, order.
+__global__ __launch_bounds__(kSortThreads) void priority_small_kernel(
+    const int32_t *__restrict__ inverse, const float *__restrict__ phi,
+    const int32_t *__restrict__ first_index, const float *__restrict__ s_hat,
+    const uint8_t *__restrict__ heavy, int64_t R, int64_t n_unique,
+    const int64_t *__restrict__ nu_dev, int64_t cap, double alpha, double gamma, double delta,
+    double eps, double *__restrict__ phi_out, double *__restrict__ pi_out,
+    int32_t *__restrict__ order) {
+  __shared__ unsigned long long units[kSortChunk];
+  __shared__ SortItem sh[kSortChunk];
+  const int64_t nu = read_nu(n_unique, nu_dev, cap);   // <= cap <= kSortChunk
+  const int tid = threadIdx.x;
+  for (int g = tid; g < nu; g += kSortThreads) units[g] = 0ull;
+  __syncthreads();
+  for (int64_t i = tid; i < R; i += kSortThreads) {
+    const int32_t g = inverse[i];
+    if (g < 0 || g >= nu) continue;
+    const uint64_t u = phi_units(phi[i]);
+    if (u) atomicAdd(&units[g], (unsigned long long)u);
+  }
+  __syncthreads();
+  int p2 = 1;
+  while (p2 < nu) p2 <<= 1;
+  for (int g = tid; g < p2; g += kSortThreads)
+    sh[g] = g < nu ? node_priority(units[g], g, first_index, s_hat, heavy, R, alpha, gamma,
+                                   delta, eps, phi_out, pi_out)
+                   : pad_item();
+  __syncthreads();
+  bitonic_lds(sh, p2);
+  for (int g = tid; g < nu; g += kSortThreads) order[g] = (int32_t)sh[g].g;
+}
+
+// Unit sums for many requests: each workgroup adds up rounds of
+// kAggRound consecutive requests in an LDS table keyed by fused node (hot
+// nodes of a Zipf mix appear many times per round), then adds each entry to
+// the global sums with one atomic.
+constexpr int kAggRound = 1024, kAggSlots = 2048;
+__global__ __launch_bounds__(kPrioThreads) void priority_sum_agg_kernel(
+    const int32_t *__restrict__ inverse, const float *__restrict__ phi, int64_t R,
+    int64_t n_unique, const int64_t *__restrict__ nu_dev, int64_t cap,
+    uint64_t *__restrict__ units) {
+  __shared__ int32_t tkey[kAggSlots];
+  __shared__ unsigned long long tval[kAggSlots];
+  const int64_t nu = read_nu(n_unique, nu_dev, cap);
+  const int tid = threadIdx.x;
+  for (int64_t r0 = (int64_t)blockIdx.x * kAggRound; r0 < R;
+       r0 += (int64_t)gridDim.x * kAggRound) {
+    for (int j = tid; j < kAggSlots; j += kPrioThreads) {
+      tkey[j] = -1;
+      tval[j] = 0ull;
+    }
+    __syncthreads();
+    for (int j = tid; j < kAggRound; j += kPrioThreads) {
+      const int64_t i = r0 + j;
+      if (i >= R) break;
+      const int32_t g = inverse[i];
+      if (g < 0 || g >= nu) continue;
+      const uint64_t u = phi_units(phi[i]);
+      if (!u) continue;
+      // open addressing; at most kAggRound keys in kAggSlots slots
+      uint32_t h = ((uint32_t)g * 2654435761u) & (kAggSlots - 1);
+      for (;;) {
+        const int32_t prev = atomicCAS(&tkey[h], -1, g);
+        if (prev == -1 || prev == g) break;
+        h = (h + 1) & (kAggSlots - 1);
+      }
+      atomicAdd(&tval[h], (unsigned long long)u);
+    }
+    __syncthreads();
+    for (int j = tid; j < kAggSlots; j += kPrioThreads)
+      if (tkey[j] >= 0 && tval[j])
+        atomicAdd((unsigned long long *)&units[tkey[j]], tval[j]);
+    __syncthreads();
+  }
+}
+
 __global__ void priority_clear_kernel(uint64_t *__restrict__ units, int64_t n_unique,
                                       const int64_t *__restrict__ nu_dev, int64_t cap) {
   const int64_t nu = read_nu(n_unique, nu_dev, cap);
   for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < nu;
        g += (int64_t)gridDim.x * blockDim.x)
     units[g] = 0ull;
-}
-
-__global__ void priority_sum_kernel(const int32_t *__restrict__ inverse,
-                                    const float *__restrict__ phi, int64_t R, int64_t n_unique,
-                                    const int64_t *__restrict__ nu_dev, int64_t cap,
-                                    uint64_t *__restrict__ units) {
-  const int64_t nu = read_nu(n_unique, nu_dev, cap);
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < R;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int32_t g = inverse[i];
-    if (g < 0 || g >= nu) continue;
-    float f = phi[i];
-    f = f > 0.0f ? f : 0.0f;                         // negative and NaN -> 0
-    f = f < 65536.0f ? f : 65535.99609375f;          // largest fp32 below 2^16
-    // f * 2^24 is exact in fp32; truncation gives the units (< 2^40)
-    const uint64_t u = (uint64_t)__float2ll_rz(f * 16777216.0f);
-    if (u) atomicAdd((unsigned long long *)&units[g], (unsigned long long)u);
-  }
 }
 
 __global__ void priority_pi_kernel(const uint64_t *__restrict__ units,
@@ -82,26 +205,9 @@ __global__ void priority_pi_kernel(const uint64_t *__restrict__ units,
                                    double *__restrict__ pi_out, SortItem *__restrict__ items) {
   const int64_t nu = read_nu(n_unique, nu_dev, cap);
   for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < nu;
-       g += (int64_t)gridDim.x * blockDim.x) {
-    // units < 2^63: one correctly rounded conversion, then an exact scaling
-    const double ph = __dmul_rn(__ll2double_rn((long long)units[g]), 1.0 / kPhiUnit);
-    const int64_t s = first_index[g];
-    const bool ok = s >= 0 && s < R;
-    const double sq = ok ? (double)s_hat[s] : 0.0;
-    const double y = ok && heavy ? (heavy[s] ? 1.0 : 0.0) : 0.0;
-    double p = __dadd_rn(__ddiv_rn(alpha, __dadd_rn(sq, eps)), __dmul_rn(gamma, ph));
-    p = __dadd_rn(p, __dmul_rn(delta, y));
-    p = p == 0.0 ? 0.0 : p;   // -0 -> +0
-    if (phi_out) phi_out[g] = ph;
-    if (pi_out) pi_out[g] = p;
-    const uint64_t b = (uint64_t)__double_as_longlong(p);
-    const uint64_t ord = (b >> 63) ? ~b : (b | 0x8000000000000000ull);   // ascending with pi
-    SortItem it;
-    it.key = ~ord;
-    it.g = (uint32_t)g;
-    it.pad = 0u;
-    items[g] = it;
-  }
+       g += (int64_t)gridDim.x * blockDim.x)
+    items[g] = node_priority(units[g], g, first_index, s_hat, heavy, R, alpha, gamma, delta, eps,
+                             phi_out, pi_out);
 }
 
 // Bitonic sort of each kSortChunk-item chunk of the first n_u items.
@@ -116,33 +222,9 @@ __global__ __launch_bounds__(kSortThreads) void priority_chunk_sort_kernel(
   int p2 = 1;
   while (p2 < n) p2 <<= 1;
   const int tid = threadIdx.x;
-  for (int i = tid; i < p2; i += kSortThreads) {
-    if (i < n) {
-      sh[i] = items[c0 + i];
-    } else {
-      SortItem pad;
-      pad.key = ~0ull;
-      pad.g = 0xffffffffu;
-      pad.pad = 0u;
-      sh[i] = pad;
-    }
-  }
+  for (int i = tid; i < p2; i += kSortThreads) sh[i] = i < n ? items[c0 + i] : pad_item();
   __syncthreads();
-  for (int size = 2; size <= p2; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = tid; i < p2 / 2; i += kSortThreads) {
-        const int lo = 2 * i - (i & (stride - 1));
-        const int hi = lo + stride;
-        const bool up = (lo & size) == 0;
-        const SortItem a = sh[lo], b = sh[hi];
-        if (item_less(b, a) == up) {
-          sh[lo] = b;
-          sh[hi] = a;
-        }
-      }
-      __syncthreads();
-    }
-  }
+  bitonic_lds(sh, p2);
   for (int i = tid; i < n; i += kSortThreads) items[c0 + i] = sh[i];
 }
 
@@ -205,6 +287,12 @@ hipError_t launch_priority(const int32_t *inverse, const int32_t *first_index, i
                            double alpha, double gamma, double delta, double eps, double *phi_out,
                            double *pi_out, int32_t *order, void *ws, hipStream_t st) {
   const int64_t n = n_unique >= 0 ? n_unique : cap;   // launch bound
+  if (cap <= kSortChunk) {
+    hipLaunchKernelGGL(priority_small_kernel, dim3(1), dim3(kSortThreads), 0, st, inverse, phi,
+                       first_index, s_hat, heavy, R, n_unique, nu_dev, cap, alpha, gamma, delta,
+                       eps, phi_out, pi_out, order);
+    return hipGetLastError();
+  }
   unsigned char *base = (unsigned char *)ws;
   uint64_t *units = (uint64_t *)base;
   SortItem *buf0 = (SortItem *)(base + align256((size_t)(cap > 0 ? cap : 1) * 8));
@@ -212,7 +300,7 @@ hipError_t launch_priority(const int32_t *inverse, const int32_t *first_index, i
                               sizeof(SortItem);
   hipLaunchKernelGGL(priority_clear_kernel, dim3(grid_of(n, kPrioThreads)), dim3(kPrioThreads),
                      0, st, units, n_unique, nu_dev, cap);
-  hipLaunchKernelGGL(priority_sum_kernel, dim3(grid_of(R, kPrioThreads)), dim3(kPrioThreads), 0,
+  hipLaunchKernelGGL(priority_sum_agg_kernel, dim3(grid_of(R, kAggRound)), dim3(kPrioThreads), 0,
                      st, inverse, phi, R, n_unique, nu_dev, cap, units);
   hipLaunchKernelGGL(priority_pi_kernel, dim3(grid_of(n, kPrioThreads)), dim3(kPrioThreads), 0,
                      st, units, first_index, s_hat, heavy, R, n_unique, nu_dev, cap, alpha, gamma,

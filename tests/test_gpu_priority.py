@@ -74,7 +74,7 @@ def test_many_fused_nodes_merge_passes():
            gamma=1.0, delta=0.0, eps=1.0)
 
 
-@pytest.mark.parametrize("n_u", [1, 4095, 4096, 4097, 9000])
+@pytest.mark.parametrize("n_u", [1, 2000, 4095, 4096, 4097, 9000])
 def test_chunk_boundaries_and_ties(n_u):
     rng = np.random.default_rng(n_u)
     keys = rng.permutation(np.repeat(rng.integers(-2 ** 62, 2 ** 62, size=n_u), 2))
