@@ -89,6 +89,10 @@ def parse():
     ap.add_argument("--prio-only", default="",
                     help="only time hs_dedup + hs_priority on this workload's requests (e.g. "
                          "dedup256k; one JSON line of its own)")
+    ap.add_argument("--batch-curve", action="store_true",
+                    help="micro-batching (Eq. 8): score latency against batch size, and the "
+                         "window's distinct queries scored in sub-batches of at most B or split "
+                         "over k streams (mean / max completion); one JSON line of its own")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
     return ap.parse_args()
@@ -119,6 +123,9 @@ def main():
         return
     if args.prio_only:
         priority_bench(args)
+        return
+    if args.batch_curve:
+        batch_curve_bench(args)
         return
 
     import numpy as np
@@ -434,6 +441,116 @@ def signature_bench(args):
                                   f"(Zipf({cfg.zipf_s}) over {cfg.n_templates} templates), "
                                   "normalised query text + Top-K parameter"},
            "roofline": st["roofline"], "signature_step": st}
+    print(json.dumps(out), flush=True)
+
+
+def batch_curve_bench(args):
+    """Latency of the score step (hs_score_topk) against the number of
+    queries in one batch, and the window's distinct queries as sequential
+    sub-batches of at most B queries (B_r) or as k sub-batches on k streams
+    (k_v), with the mean and the largest query completion time (the two terms
+    of Eq. 8's objective)."""
+    import numpy as np
+    import torch
+
+    import paper_2607_22578_amd as hs
+    import synth
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.make(args.workload)
+    cfg = w.cfg
+    R, d, N, k = w.R, w.dim, w.n_corpus, w.k
+    cdt = {"bf16": hs.HS_BF16, "fp8": hs.HS_FP8_E4M3}[cfg.c_enc]
+
+    def to_dev(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    keys, q_req, corpus = to_dev(w.keys), to_dev(w.q_req), to_dev(w.corpus)
+    scale = to_dev(w.scale) if w.scale is not None else None
+    m = hs.MergedRetrieval(R, d, N, k, hs.HS_BF16, cdt, device=dev)
+    stream = torch.cuda.Stream(dev)
+    nu = m.dedup(keys, stream, host_count=True)
+    reps = max(3, min(args.steps, 20))
+
+    def timed(fn):
+        out = []
+        for r in range(reps + 2):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize(dev)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            torch.cuda.synchronize(dev)
+            if r >= 2:
+                out.append(a.elapsed_time(b))
+        return float(np.median(out))
+
+    # latency against batch size: the first b request rows as the batch
+    m.q_unique[:R].copy_(q_req)
+    torch.cuda.synchronize(dev)
+    curve = []
+    for b in [1, 2, 4, 8, 16, 32, 64, 96, 128, 160, 256, 384, 512, 1024, 2048]:
+        if b > R:
+            break
+        ms = timed(lambda: hs.hs_score_topk(m.plan, m.q_unique, b, None, corpus, scale,
+                                            m.topk_score, m.topk_index, m.ws, stream=stream))
+        curve.append({"batch": b, "ms": round(ms, 4), "queries_per_s": round(b / ms * 1e3, 1)})
+
+    # the window's distinct queries in sub-batches of at most B, one after another
+    m.gather_queries(q_req, stream)
+    torch.cuda.synchronize(dev)
+    chunked = []
+    for B in sorted({16, 32, 64, 128, 256, nu}):
+        if B > nu:
+            continue
+        runs = []
+        for r in range(reps):
+            evs = []
+            m.score_chunked(corpus, nu, B, scale, stream, events=evs)
+            torch.cuda.synchronize(dev)
+            t0 = evs[0][0]
+            done = [t0.elapsed_time(e[1]) for e in evs]
+            sizes = [min(B, nu - j * B) for j in range(len(evs))]
+            mean_c = sum(c * s for c, s in zip(done, sizes)) / nu
+            runs.append((mean_c, done[-1]))
+        mean_c = float(np.median([x[0] for x in runs]))
+        max_c = float(np.median([x[1] for x in runs]))
+        chunked.append({"B": B, "sub_batches": -(-nu // B), "mean_completion_ms": round(mean_c, 4),
+                        "max_completion_ms": round(max_c, 4),
+                        "J_lambda_0.5_ms": round(0.5 * mean_c + 0.5 * max_c, 4)})
+
+    # k sub-batches on k streams (each with its own workspace)
+    split = []
+    for parts in (1, 2, 4):
+        streams = [torch.cuda.Stream(dev) for _ in range(parts)]
+        res = []
+        for r in range(reps):
+            torch.cuda.synchronize(dev)
+            a = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for s_ in streams:
+                s_.wait_event(a)
+            m.score_split(corpus, nu, parts, streams, scale)
+            ends = []
+            for s_ in streams:
+                e = torch.cuda.Event(enable_timing=True)
+                e.record(s_)
+                ends.append(e)
+            torch.cuda.synchronize(dev)
+            res.append(max(a.elapsed_time(e) for e in ends))
+        split.append({"k": parts, "makespan_ms": round(float(np.median(res)), 4)})
+
+    full = next(c for c in chunked if c["B"] == nu)
+    out = {"metric": "score latency vs batch size and micro-batching of the window (Eq. 8)",
+           "value": round(nu / full["max_completion_ms"] * 1e3, 1), "unit": "queries/s",
+           "n_gpus": 1, "steps": reps, "warmup": 2, "ms_per_step": full["max_completion_ms"],
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic",
+           "config": {"workload": f"{cfg.name}: {cfg.desc}", "n_unique": nu, "k": k,
+                      "n_corpus": N},
+           "latency_curve": curve, "sequential_sub_batches": chunked, "stream_split": split}
     print(json.dumps(out), flush=True)
 
 

@@ -408,3 +408,49 @@ class MergedRetrieval:
                     heavy, alpha, gamma, delta, eps, self.phi_fused, self.pi, self.order, self.ws,
                     stream=stream)
 
+    # ------------------------------------------------ micro-batching (Eq. 8)
+
+    def score_chunked(self, corpus, n_unique: int, chunk: int, scale=None, stream=None,
+                      events=None):
+        """Scores the window's n_unique distinct queries (host count) as
+        consecutive sub-batches of at most `chunk` queries, one after the
+        other on `stream` (the batch limit B_r of Appendix A; small batches
+        finish their queries earlier).  Results land in topk_score/index as
+        for one batch.  `events`, if given, is a list that receives one
+        (start, end) event pair per sub-batch."""
+        import torch
+        row_q = self.q_row_bytes
+        for b0 in range(0, n_unique, chunk):
+            nb = min(chunk, n_unique - b0)
+            if events is not None:
+                ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                ev[0].record(stream)
+            q = self.q_unique.data_ptr() + b0 * row_q
+            ts = self.topk_score.data_ptr() + b0 * self.k * 4
+            ti = self.topk_index.data_ptr() + b0 * self.k * 4
+            hs_score_topk(self.plan, q, nb, None, corpus, scale, ts, ti, self.ws, stream=stream)
+            if events is not None:
+                ev[1].record(stream)
+                events.append(ev)
+
+    def score_split(self, corpus, n_unique: int, parts: int, streams, scale=None):
+        """Scores the distinct queries as `parts` near-equal sub-batches, each
+        on its own stream with its own workspace (the split k_v of Appendix
+        A: sub-batches that may run side by side).  The caller orders the
+        streams after the current producer and synchronises them."""
+        import torch
+        if not hasattr(self, "_split_ws") or len(self._split_ws) < parts:
+            self._split_ws = [torch.empty_like(self.ws) for _ in range(parts)]
+        row_q = self.q_row_bytes
+        base = 0
+        for j in range(parts):
+            nb = n_unique // parts + (1 if j < n_unique % parts else 0)
+            if nb == 0:
+                continue
+            q = self.q_unique.data_ptr() + base * row_q
+            ts = self.topk_score.data_ptr() + base * self.k * 4
+            ti = self.topk_index.data_ptr() + base * self.k * 4
+            hs_score_topk(self.plan, q, nb, None, corpus, scale, ts, ti, self._split_ws[j],
+                          stream=streams[j])
+            base += nb
+
