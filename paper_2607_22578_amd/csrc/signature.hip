@@ -19,9 +19,10 @@
 // big-endian, as a signed (two's-complement) integer.
 //
 // One thread per node: SHA-256 is sequential within a message, and a window
-// holds thousands of nodes.  The thread streams its message bytes through a
-// 16-word shift register (static register indexing only) and compresses every
-// 64 bytes (FIPS 180-4, Sec. 6.2).  Byte sources are read 16 bytes at a time
+// holds thousands of nodes.  A workgroup first copies its nodes' text and
+// parameter bytes into LDS; each thread then writes its message into its own
+// LDS column, in rounds of three 64-byte blocks, and compresses each round's
+// blocks (FIPS 180-4, Sec. 6.2).  Byte sources are read 16 bytes at a time
 // through buffer descriptors, so reads past a buffer's end return zeros and
 // never touch memory.
 #include "common.h"
@@ -90,21 +91,6 @@ __device__ __forceinline__ void sha256_block(uint32_t h[8], uint32_t w[16]) {
   h[7] += hh;
 }
 
-// Byte at `pos` of a 16-byte window held as four little-endian words.
-__device__ __forceinline__ uint32_t win_byte(const uint32_t win[4], uint32_t pos) {
-  const uint32_t q = (pos >> 2) & 3u;
-  const uint32_t wd = q == 0 ? win[0] : q == 1 ? win[1] : q == 2 ? win[2] : win[3];
-  return (wd >> ((pos & 3u) * 8u)) & 0xffu;
-}
-
-__device__ __forceinline__ bool ascii_space(uint32_t c) {
-  return c == 0x20u || (c >= 0x09u && c <= 0x0du);
-}
-
-__device__ __forceinline__ uint32_t ascii_lower(uint32_t c) {
-  return (c >= 0x41u && c <= 0x5au) ? c + 0x20u : c;
-}
-
 // 16 bytes at the 16-aligned offset `off` of a buffer of `nbytes`; bytes past
 // the end read as zero.  The last partial block is read byte by byte (a
 // 16-byte buffer load that straddles the end may return zeros for all of it).
@@ -161,10 +147,9 @@ __device__ __forceinline__ void clamp_range(const int64_t *off, int64_t i, uint3
 constexpr int kSigThreads = 128;
 // LDS staging of one group's text and parameter bytes
 constexpr uint32_t kStageText = 16 * 1024, kStageParam = 2 * 1024;
-// Messages of at most kMsgMax bytes (three blocks with the padding) are built
-// whole in LDS, one column of kMsgWords words per thread, and compressed from
-// there; longer ones are streamed.
-constexpr uint32_t kMsgWords = 48, kMsgMax = kMsgWords * 4 - 9;
+// Messages are built in LDS in rounds of kRound bytes (three SHA-256 blocks),
+// one column of kRound / 4 words per thread.
+constexpr uint32_t kRound = 192;
 
 // Stages [sb, sb + sl) of a buffer of `nbytes` (sb, sl multiples of 16) into
 // LDS with coalesced 16-byte loads, eight in flight per thread; the one block
@@ -225,7 +210,7 @@ __global__ __launch_bounds__(kSigThreads) void signature_kernel(SigArgs a) {
       __builtin_amdgcn_make_buffer_rsrc((void *)a.digest, (short)0, (int)dig_bytes, 0x00020000);
   __shared__ uint4 s_text[kStageText / 16];
   __shared__ uint4 s_par[kStageParam / 16];
-  __shared__ uint32_t s_msg[kMsgWords * kSigThreads];
+  __shared__ uint32_t s_msg[kRound / 4 * kSigThreads];
   const int64_t vend = a.first + a.count;
 
   // Groups of kSigThreads consecutive nodes.  Their texts (and parameters)
@@ -272,7 +257,7 @@ __global__ __launch_bounds__(kSigThreads) void signature_kernel(SigArgs a) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) h[i] = kSha256H0[i];
 
-    if (16u + P + (t1 - t0) + 32u * m <= kMsgMax) {
+    if (16u + P + (t1 - t0) + 32u * m + 9u <= kRound) {
       // Short message: write it into this thread's LDS column (word j at
       // s_msg[j * kSigThreads + tid], bytes in message order within a word),
       // then compress its blocks.  The column layout keeps every LDS access
@@ -287,7 +272,7 @@ __global__ __launch_bounds__(kSigThreads) void signature_kernel(SigArgs a) {
         for (int i = 0; i < 4; ++i) put8(o + i, (x >> (8 * i)) & 0xffu);
       };
 #pragma unroll
-      for (uint32_t j = 0; j < kMsgWords; ++j) s_msg[j * kSigThreads + tid] = 0u;
+      for (uint32_t j = 0; j < kRound / 4; ++j) s_msg[j * kSigThreads + tid] = 0u;
       s_msg[tid] = tau;                    // le32(tau), bytes 0..3
       s_msg[kSigThreads + tid] = P;        // le32(|Theta|), bytes 4..7
       // Bytes are consumed one aligned 16-byte window at a time (every lane
@@ -364,123 +349,145 @@ __global__ __launch_bounds__(kSigThreads) void signature_kernel(SigArgs a) {
         sha256_block(h, w);
       }
     } else {
+      // Longer message: the same column, filled and compressed in rounds.
+      // The message is built in this thread's LDS column in rounds of
+      // kRound bytes (word j of a round at s_msg[j * kSigThreads + tid], bytes
+      // in message order within a word; the column layout keeps every LDS
+      // access of a wave on distinct banks), and each round's blocks are then
+      // compressed.  Every writer places bytes by their message position and
+      // a round keeps those inside it.  Source bytes are consumed one aligned
+      // 16-byte window at a time (every lane takes its k-th window in the same
+      // iteration), with the window's bytes unrolled.
+      uint8_t *col = (uint8_t *)s_msg;
+      const int tid = threadIdx.x;
+      uint32_t r0 = 0, r_end = 0;
+      auto put8 = [&](uint32_t o, uint32_t b) {
+        if (o >= r0 && o < r_end)
+          col[(((o - r0) >> 2) * kSigThreads + tid) * 4 + (o & 3u)] = (uint8_t)b;
+      };
+      auto put32 = [&](uint32_t o, uint32_t x) {
+  #pragma unroll
+        for (int i = 0; i < 4; ++i) put8(o + i, (x >> (8 * i)) & 0xffu);
+      };
 
-    // pass 1: length of D
-    uint32_t D = t1 - t0;
-    if (NORM) {
-      D = 0;
-      bool gap = false;
-      for (uint32_t r = t0; r < t1; ++r) {
-        if (r == t0 || (r & 15u) == 0)
-          fetch_window(t_lds, s_text, tsb, rt, r & ~15u, a.text_bytes, win);
-        const uint32_t c = win_byte(win, r);
-        if (ascii_space(c)) {
-          gap = true;
+      // |D| comes before D in the message: with normalisation, count it first
+      uint32_t D = t1 - t0;
+      if (NORM) {
+        D = 0;
+        uint32_t gap = 0;
+        for (uint32_t base = t0 & ~15u; base < t1; base += 16u) {
+          fetch_window(t_lds, s_text, tsb, rt, base, a.text_bytes, win);
+  #pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const uint32_t r = base + i;
+            const uint32_t c = (win[i >> 2] >> (8 * (i & 3))) & 0xffu;
+            const uint32_t in = (uint32_t)(r >= t0) & (uint32_t)(r < t1);
+            const uint32_t sp = (uint32_t)(c == 0x20u) | (uint32_t)(c - 0x09u < 5u);
+            const uint32_t keep = in & (sp ^ 1u);
+            D += keep & gap & (uint32_t)(D > 0u);
+            D += keep;
+            gap = (in & sp) | (gap & (in ^ 1u));
+          }
+        }
+      }
+      const uint32_t o0 = 12u + P;                  // first byte of D
+      const uint32_t L = 16u + P + D + 32u * m;     // message bytes
+      const uint32_t end = ((L + 8u) / 64u + 1u) * 64u;
+      const uint64_t bits = (uint64_t)L * 8u;
+      // resume point of the normalised text: start of the last window taken
+      uint32_t n_base = t0 & ~15u, n_o = o0, n_gap = 0;
+
+      for (r0 = 0; r0 < end; r0 += kRound) {
+        r_end = r0 + kRound < end ? r0 + kRound : end;
+  #pragma unroll
+        for (uint32_t j = 0; j < kRound / 4; ++j) s_msg[j * kSigThreads + tid] = 0u;
+        put32(0u, tau);
+        put32(4u, P);
+        // parameters: message bytes 8 .. 8 + P (only the windows this round needs)
+        if (8u + P > r0 && 8u < r_end) {
+          const uint32_t i0 = r0 > 8u ? r0 - 8u : 0u;
+          const uint32_t i1 = r_end - 8u < P ? r_end - 8u : P;
+          for (uint32_t base = (p0 + i0) & ~15u; base < p0 + i1; base += 16u) {
+            fetch_window(p_lds, s_par, psb, rp, base, a.param_bytes, win);
+  #pragma unroll
+            for (int i = 0; i < 16; ++i) {
+              const uint32_t r = base + i;
+              if (r >= p0 && r < p1) put8(8u + r - p0, (win[i >> 2] >> (8 * (i & 3))) & 0xffu);
+            }
+          }
+        }
+        if (!NORM) {
+          if (o0 + D > r0 && o0 < r_end) {
+            const uint32_t i0 = r0 > o0 ? r0 - o0 : 0u;
+            const uint32_t i1 = r_end - o0 < D ? r_end - o0 : D;
+            for (uint32_t base = (t0 + i0) & ~15u; base < t0 + i1; base += 16u) {
+              fetch_window(t_lds, s_text, tsb, rt, base, a.text_bytes, win);
+  #pragma unroll
+              for (int i = 0; i < 16; ++i) {
+                const uint32_t r = base + i;
+                if (r >= t0 && r < t1) put8(o0 + r - t0, (win[i >> 2] >> (8 * (i & 3))) & 0xffu);
+              }
+            }
+          }
         } else {
-          D += (gap && D > 0) ? 2u : 1u;
-          gap = false;
+          // Each byte is written at the output position whether or not it is
+          // kept; the position only advances past kept bytes, so a byte that
+          // is not kept is overwritten by the next one (or by the field that
+          // follows D).  A window that runs past the round is taken again,
+          // from the state saved at its start, by the next round.
+          uint32_t base = n_base, o = n_o, gap = n_gap;
+          while (base < t1 && o < r_end) {
+            n_base = base;
+            n_o = o;
+            n_gap = gap;
+            fetch_window(t_lds, s_text, tsb, rt, base, a.text_bytes, win);
+  #pragma unroll
+            for (int i = 0; i < 16; ++i) {
+              const uint32_t r = base + i;
+              const uint32_t c = (win[i >> 2] >> (8 * (i & 3))) & 0xffu;
+              // (bitwise & and | on the flags: no short-circuit branches)
+              const uint32_t in = (uint32_t)(r >= t0) & (uint32_t)(r < t1);
+              const uint32_t sp = (uint32_t)(c == 0x20u) | (uint32_t)(c - 0x09u < 5u);
+              const uint32_t keep = in & (sp ^ 1u);
+              // a kept byte after a gap is preceded by one space, unless it is
+              // the first byte of D
+              put8(o, 0x20u);
+              o += keep & gap & (uint32_t)(o > o0);
+              put8(o, c + ((uint32_t)(c - 0x41u < 26u) << 5));
+              o += keep;
+              gap = (in & sp) | (gap & (in ^ 1u));
+            }
+            base += 16u;
+          }
+        }
+        put32(8u + P, D);
+        put32(o0 + D, m);
+        // predecessor digests: message bytes 16 + P + D + 32 j
+        for (uint32_t j = 0; j < m; ++j) {
+          const uint32_t oj = 16u + P + D + 32u * j;
+          if (oj + 32u <= r0 || oj >= r_end) continue;
+          const int64_t u = a.pred_idx[q0 + j];
+          uint32_t d8[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+          if (u >= 0 && u < a.first) {
+            load_window(rd, (uint32_t)u * 32u, dig_bytes, d8);
+            load_window(rd, (uint32_t)u * 32u + 16u, dig_bytes, d8 + 4);
+          }
+  #pragma unroll
+          for (int i = 0; i < 8; ++i) put32(oj + 4 * i, d8[i]);
+        }
+        put8(L, 0x80u);
+        // last 8 bytes: the bit length, big-endian (the high three are zero)
+  #pragma unroll
+        for (int i = 3; i < 8; ++i) put8(end - 8u + i, (uint32_t)(bits >> (8 * (7 - i))) & 0xffu);
+        for (uint32_t bk = 0; bk < (r_end - r0) / 64u; ++bk) {
+          uint32_t w[16];
+  #pragma unroll
+          for (int i = 0; i < 16; ++i)
+            w[i] = __builtin_bswap32(s_msg[(bk * 16u + i) * kSigThreads + tid]);
+          sha256_block(h, w);
         }
       }
     }
-
-    // pass 2: stream the message (plus FIPS 180-4 padding) through the block
-    const uint32_t L = 16u + P + D + 32u * m;
-    const uint32_t nblk = (L + 8u) / 64u + 1u;
-    const uint32_t end = nblk * 64u;
-    const uint64_t bits = (uint64_t)L * 8u;
-    const uint32_t sP = 8u, sDl = 8u + P, sD = 12u + P, sM = 12u + P + D, sQ = 16u + P + D;
-    uint32_t w[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) w[i] = 0u;
-    uint32_t cur = 0u;
-    uint32_t rp_pos = p0, rt_pos = t0, wbase = 0xffffffffu;   // window state
-    int src = -1;                                            // 0 params, 1 text, 2 digests
-    bool gap = false;
-    uint32_t emitted = 0u;
-    int64_t pi = -1;   // current predecessor
-    // Blocks in an outer loop, bytes in an inner one: the compression stays
-    // out of the byte loop, whose body is then only the byte source and the
-    // shift into the block's words.
-    for (uint32_t pos = 0; pos < end;) {
-     for (uint32_t i = 0; i < 64u; ++i, ++pos) {
-      uint32_t b;
-      if (pos < sP) {
-        b = ((pos < 4u ? tau : P) >> ((pos & 3u) * 8u)) & 0xffu;
-      } else if (pos < sDl) {
-        if (src != 0 || (rp_pos & ~15u) != wbase) {
-          wbase = rp_pos & ~15u;
-          fetch_window(p_lds, s_par, psb, rp, wbase, a.param_bytes, win);
-          src = 0;
-        }
-        b = win_byte(win, rp_pos);
-        ++rp_pos;
-      } else if (pos < sD) {
-        b = (D >> ((pos - sDl) * 8u)) & 0xffu;
-      } else if (pos < sM) {
-        // next byte of D: raw, or normalised (a pending gap emits one space
-        // before the next non-space byte; leading spaces never emit one)
-        for (;;) {
-          if (src != 1 || (rt_pos & ~15u) != wbase) {
-            wbase = rt_pos & ~15u;
-            fetch_window(t_lds, s_text, tsb, rt, wbase, a.text_bytes, win);
-            src = 1;
-          }
-          const uint32_t c = win_byte(win, rt_pos);
-          if (!NORM) {
-            b = c;
-            ++rt_pos;
-            break;
-          }
-          if (ascii_space(c)) {
-            gap = true;
-            ++rt_pos;
-            continue;
-          }
-          if (gap && emitted > 0u) {
-            b = 0x20u;   // the space; c is emitted next time
-            gap = false;
-          } else {
-            b = ascii_lower(c);
-            gap = false;
-            ++rt_pos;
-          }
-          break;
-        }
-        ++emitted;
-      } else if (pos < sQ) {
-        b = (m >> ((pos - sM) * 8u)) & 0xffu;
-      } else if (pos < L) {
-        const uint32_t j = pos - sQ;
-        if ((j & 31u) == 0u) pi = a.pred_idx[q0 + (j >> 5)];
-        if (pi >= 0 && pi < a.first) {
-          const uint32_t off = (uint32_t)pi * 32u + (j & 31u);
-          if (src != 2 || (off & ~15u) != wbase) {
-            wbase = off & ~15u;
-            load_window(rd, wbase, dig_bytes, win);
-            src = 2;
-          }
-          b = win_byte(win, off);
-        } else {
-          b = 0u;   // a predecessor outside [0, first) hashes as 32 zero bytes
-        }
-      } else if (pos == L) {
-        b = 0x80u;
-      } else if (pos >= end - 8u) {
-        b = (uint32_t)(bits >> ((end - 1u - pos) * 8u)) & 0xffu;
-      } else {
-        b = 0u;
-      }
-      cur = (cur << 8) | b;
-      if ((i & 3u) == 3u) {
-#pragma unroll
-        for (int j = 0; j < 15; ++j) w[j] = w[j + 1];
-        w[15] = cur;
-        cur = 0u;
-      }
-     }
-     sha256_block(h, w);
-    }
-    }   // long message
 
     uint4 *dst = (uint4 *)(a.digest + v * 32);
     dst[0] = make_uint4(__builtin_bswap32(h[0]), __builtin_bswap32(h[1]),
