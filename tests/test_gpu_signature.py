@@ -196,3 +196,27 @@ def test_group_text_beyond_the_lds_copy():
     op = np.full(60, 4, dtype=np.uint32)
     _check(op, None, None, t, toff, None, None, [(0, 60)], True)
     _check(op, None, None, t, toff, None, None, [(0, 60)], False)
+
+
+def test_long_parameters_and_digests_across_rounds():
+    # parameter blobs longer than a 192-byte round, texts around a round,
+    # and up to 9 predecessor digests, so that every field of the message
+    # can straddle a round boundary
+    rng = np.random.default_rng(12)
+    n0, n1 = 50, 150
+    n = n0 + n1
+    params = [bytes(rng.integers(0, 256, size=int(rng.integers(0, 700)), dtype=np.uint8))
+              for _ in range(n)]
+    texts = [bytes(rng.choice(np.frombuffer(b"aB \t\nxyZ", np.uint8),
+                              size=int(rng.integers(0, 400)))) for _ in range(n)]
+    preds, qoff = [], [0]
+    for v in range(n):
+        if v >= n0:
+            preds += [int(u) for u in rng.integers(0, n0, size=int(rng.integers(0, 10)))]
+        qoff.append(len(preds))
+    p, poff = _pack(params)
+    t, toff = _pack(texts)
+    op = rng.integers(0, 50, size=n).astype(np.uint32)
+    for norm in (True, False):
+        _check(op, p, poff, t, toff, np.array(qoff, np.int32), np.array(preds, np.int32),
+               [(0, n0), (n0, n1)], norm)
