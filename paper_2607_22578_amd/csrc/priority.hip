@@ -32,8 +32,10 @@
 namespace hs {
 
 constexpr int kPrioThreads = 256;
-constexpr int kSortChunk = 4096;
-constexpr int kSortThreads = 1024;
+constexpr int kSmallMax = 4096;      // fused nodes handled by one workgroup
+constexpr int kSmallThreads = 1024;
+constexpr int kSortChunk = 1024;     // items per chunk of the many-node sort
+constexpr int kSortThreads = 512;
 constexpr double kPhiUnit = 16777216.0;   // 2^24 units per 1.0
 
 struct SortItem {
@@ -83,6 +85,13 @@ __device__ __forceinline__ SortItem node_priority(uint64_t units, int64_t g,
 }
 
 // In-place ascending bitonic sort of sh[0, p2) (p2 a power of two, padded).
+// Pair i of a stage joins items lo = 2i - (i mod stride) and lo + stride; a
+// wave takes pairs [64 w, 64 w + 64) (and the same range one workgroup size
+// further on, and so on), whose items lie in its own 128-item blocks
+// whenever stride <= 64.  Such
+// stages only need the wave's own LDS accesses ordered (a wavefront fence);
+// a workgroup barrier follows the stages with larger strides and the last
+// stage of each size.
 __device__ __forceinline__ void bitonic_lds(SortItem *sh, int p2) {
   const int tid = threadIdx.x;
   for (int size = 2; size <= p2; size <<= 1) {
@@ -97,10 +106,17 @@ __device__ __forceinline__ void bitonic_lds(SortItem *sh, int p2) {
           sh[hi] = a;
         }
       }
-      __syncthreads();
+      if (stride > 64 || stride == 1) {
+        __syncthreads();
+      } else {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      }
     }
   }
 }
+static_assert(kSortThreads % 64 == 0 && kSmallThreads % 64 == 0, "whole waves");
 
 __device__ __forceinline__ SortItem pad_item() {
   SortItem pad;
@@ -110,22 +126,22 @@ __device__ __forceinline__ SortItem pad_item() {
   return pad;
 }
 
-// The whole step in one workgroup when at most kSortChunk fused nodes are
+// The whole step in one workgroup when at most kSmallMax fused nodes are
 // possible: unit sums in LDS (64-bit LDS atomics), priorities, sort, order.
-__global__ __launch_bounds__(kSortThreads) void priority_small_kernel(
+__global__ __launch_bounds__(kSmallThreads) void priority_small_kernel(
     const int32_t *__restrict__ inverse, const float *__restrict__ phi,
     const int32_t *__restrict__ first_index, const float *__restrict__ s_hat,
     const uint8_t *__restrict__ heavy, int64_t R, int64_t n_unique,
     const int64_t *__restrict__ nu_dev, int64_t cap, double alpha, double gamma, double delta,
     double eps, double *__restrict__ phi_out, double *__restrict__ pi_out,
     int32_t *__restrict__ order) {
-  __shared__ unsigned long long units[kSortChunk];
-  __shared__ SortItem sh[kSortChunk];
-  const int64_t nu = read_nu(n_unique, nu_dev, cap);   // <= cap <= kSortChunk
+  __shared__ unsigned long long units[kSmallMax];
+  __shared__ SortItem sh[kSmallMax];
+  const int64_t nu = read_nu(n_unique, nu_dev, cap);   // <= cap <= kSmallMax
   const int tid = threadIdx.x;
-  for (int g = tid; g < nu; g += kSortThreads) units[g] = 0ull;
+  for (int g = tid; g < nu; g += kSmallThreads) units[g] = 0ull;
   __syncthreads();
-  for (int64_t i = tid; i < R; i += kSortThreads) {
+  for (int64_t i = tid; i < R; i += kSmallThreads) {
     const int32_t g = inverse[i];
     if (g < 0 || g >= nu) continue;
     const uint64_t u = phi_units(phi[i]);
@@ -134,13 +150,13 @@ __global__ __launch_bounds__(kSortThreads) void priority_small_kernel(
   __syncthreads();
   int p2 = 1;
   while (p2 < nu) p2 <<= 1;
-  for (int g = tid; g < p2; g += kSortThreads)
+  for (int g = tid; g < p2; g += kSmallThreads)
     sh[g] = g < nu ? node_priority(units[g], g, first_index, s_hat, heavy, R, alpha, gamma,
                                    delta, eps, phi_out, pi_out)
                    : pad_item();
   __syncthreads();
   bitonic_lds(sh, p2);
-  for (int g = tid; g < nu; g += kSortThreads) order[g] = (int32_t)sh[g].g;
+  for (int g = tid; g < nu; g += kSmallThreads) order[g] = (int32_t)sh[g].g;
 }
 
 // Unit sums for many requests: each workgroup adds up rounds of
@@ -287,8 +303,8 @@ hipError_t launch_priority(const int32_t *inverse, const int32_t *first_index, i
                            double alpha, double gamma, double delta, double eps, double *phi_out,
                            double *pi_out, int32_t *order, void *ws, hipStream_t st) {
   const int64_t n = n_unique >= 0 ? n_unique : cap;   // launch bound
-  if (cap <= kSortChunk) {
-    hipLaunchKernelGGL(priority_small_kernel, dim3(1), dim3(kSortThreads), 0, st, inverse, phi,
+  if (cap <= kSmallMax) {
+    hipLaunchKernelGGL(priority_small_kernel, dim3(1), dim3(kSmallThreads), 0, st, inverse, phi,
                        first_index, s_hat, heavy, R, n_unique, nu_dev, cap, alpha, gamma, delta,
                        eps, phi_out, pi_out, order);
     return hipGetLastError();
