@@ -127,6 +127,9 @@ def main():
     if args.batch_curve:
         batch_curve_bench(args)
         return
+    if args.workload == "dedup256k":
+        dedup_bench(args)
+        return
 
     import numpy as np
     import torch
@@ -441,6 +444,78 @@ def signature_bench(args):
                                   f"(Zipf({cfg.zipf_s}) over {cfg.n_templates} templates), "
                                   "normalised query text + Top-K parameter"},
            "roofline": st["roofline"], "signature_step": st}
+    print(json.dumps(out), flush=True)
+
+
+def dedup_bench(args):
+    """The chunk-embedding dedup workload: one step = hs_dedup of the R chunk
+    ids of all workflows + the gather of the distinct ids' embedding rows
+    (a1 + a2'); value = chunk ids per second."""
+    import numpy as np
+    import torch
+
+    import paper_2607_22578_amd as hs
+    import synth
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.make(args.workload)
+    R, d = w.R, w.dim
+    rows = w.table.shape[0]
+    plan = hs.hs_merge_plan(R, d, rows, 1, hs.HS_BF16, hs.HS_BF16)
+    ws = torch.empty(max(plan.workspace_bytes, 256), dtype=torch.uint8, device=dev)
+    kd = torch.from_numpy(w.keys).to(dev)
+    table = torch.from_numpy(w.table.view(np.int16)).view(torch.bfloat16).to(dev)
+    uk = torch.empty(R, dtype=torch.int64, device=dev)
+    fi = torch.empty(R, dtype=torch.int32, device=dev)
+    ct = torch.empty(R, dtype=torch.int32, device=dev)
+    inv = torch.empty(R, dtype=torch.int32, device=dev)
+    nu = torch.zeros(1, dtype=torch.int64, device=dev)
+    emb = torch.empty((R, d), dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.Stream(dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        hs.hs_dedup(plan, kd, uk, fi, ct, inv, nu, None, ws, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        hs.hs_scatter(table, rows, d * 2, uk, 1, R, nu, emb, stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+    n_u = int(nu.item())
+    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3))
+           for _ in range(0, args.steps, EV_EVERY)]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize(dev)
+    t0.record(stream)
+    for i in range(args.steps):
+        step(evs[i // EV_EVERY] if i % EV_EVERY == 0 else None)
+    t1.record(stream)
+    torch.cuda.synchronize(dev)
+    total = t0.elapsed_time(t1)
+    dd = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    gg = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    # algorithmic bytes: keys in; distinct keys, survivors, counts and the
+    # request map out; the distinct rows read and written once
+    alg = R * 8 + n_u * (8 + 4 + 4) + R * 4 + 2 * n_u * d * 2
+    t = (dd + gg) * 1e-3
+    out = {"metric": "chunk ids/s through dedup + embedding-row gather", "unit": "chunk ids/s",
+           "value": round(R * args.steps / (total * 1e-3), 1), "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(total / args.steps, 4), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
+           "config": {"workload": f"{w.cfg.name}: {w.cfg.desc}", "n_requests": R,
+                      "n_unique": n_u, "dim": d, "table_rows": rows},
+           "stages_ms": {"dedup": round(dd, 4), "gather": round(gg, 4)},
+           "roofline": {"bound": "hbm", "achieved": round(alg / t / 1e9, 1),
+                        "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(alg / t / 1e9 / PEAK_HBM_GBS, 4), "traffic": None,
+                        "kernel": "hs_dedup + gather_rows_kernel",
+                        "algorithmic_bytes": alg, "kernel_ms": round(dd + gg, 4)}}
     print(json.dumps(out), flush=True)
 
 

@@ -266,7 +266,8 @@ struct RadixWs {
   uint64_t *keyA, *keyB;
   int32_t *idxA, *idxB;
   uint64_t *pmin, *pmax;   // per-block min/max of mapped keys
-  uint64_t *range;         // [0] = global min, [1] = pass count
+  uint64_t *range;         // [0] = global min, [1] = radix pass count,
+                           // [2] = key values of the dense path (0: radix)
   uint32_t *hist;          // kBins x nb, digit-major
   uint32_t *bheads;        // heads per block
   int32_t *start;          // group start positions
@@ -307,7 +308,7 @@ __global__ __launch_bounds__(kRadixThreads) void radix_prep_kernel(
   }
 }
 
-__global__ __launch_bounds__(1024) void radix_range_kernel(int nb, RadixWs ws) {
+__global__ __launch_bounds__(1024) void radix_range_kernel(int R, int nb, RadixWs ws) {
   __shared__ uint64_t smin[16], smax[16];
   const int tid = threadIdx.x;
   uint64_t mn = ~0ull, mx = 0ull;
@@ -332,8 +333,11 @@ __global__ __launch_bounds__(1024) void radix_range_kernel(int nb, RadixWs ws) {
     }
     uint64_t span = mx - mn;
     int bits = span ? 64 - __clzll((long long)span) : 0;
+    // dense path when the keys take at most R values
+    const bool dense = span < (uint64_t)R;
     ws.range[0] = mn;
-    ws.range[1] = (uint64_t)((bits + kRadixBits - 1) / kRadixBits);
+    ws.range[1] = dense ? 0ull : (uint64_t)((bits + kRadixBits - 1) / kRadixBits);
+    ws.range[2] = dense ? span + 1 : 0ull;
   }
 }
 
@@ -431,6 +435,7 @@ __device__ __forceinline__ const int32_t *sorted_idx(const RadixWs &ws) {
 
 __global__ __launch_bounds__(kRadixThreads) void radix_heads_kernel(int R, RadixWs ws) {
   __shared__ uint32_t wsum[kRadixThreads / 64 + 1];
+  if (ws.range[2]) return;   // dense path
   const uint64_t *k = sorted_keys(ws);
   const int b = blockIdx.x, tid = threadIdx.x;
   uint32_t h = 0;
@@ -447,6 +452,7 @@ __global__ __launch_bounds__(kRadixThreads) void radix_compact_kernel(
     int R, RadixWs ws, int64_t *__restrict__ uk, int32_t *__restrict__ fi,
     int32_t *__restrict__ inv, int64_t *__restrict__ nu_out) {
   __shared__ uint32_t wsum[kRadixThreads / 64 + 1];
+  if (ws.range[2]) return;   // dense path
   const uint64_t *k = sorted_keys(ws);
   const int32_t *ix = sorted_idx(ws);
   const int b = blockIdx.x, tid = threadIdx.x;
@@ -489,8 +495,133 @@ __global__ __launch_bounds__(kRadixThreads) void radix_compact_kernel(
 __global__ __launch_bounds__(256) void radix_counts_kernel(int R, RadixWs ws,
                                                            const int64_t *__restrict__ nu,
                                                            int32_t *__restrict__ cnt) {
+  if (ws.range[2]) return;   // dense path
   int g = blockIdx.x * 256 + threadIdx.x;
   if (g < R && (int64_t)g < *nu) cnt[g] = ws.start[g + 1] - ws.start[g];
+}
+
+// ---------------------------------------------------------------- dense path
+//
+// When the R mapped keys take at most R values (max - min < R: e.g. chunk
+// row ids), the groups are found by direct addressing over [min, max]
+// instead of sorting: per key value v, the first request (atomic min) and the
+// group size (atomic add); a scan over the values numbers the present ones
+// in ascending key order; each request then reads its group.  Same canonical
+// outputs as the sort.  Value arrays reuse the sort's second buffers:
+// first/count in keyB (2 x int32 per value), group ids in idxB; the scan's
+// block sums use the histogram buffer.
+
+constexpr int kDenseBlk = 1024;                  // values per scan block
+constexpr int kAggRound = 1024, kAggSlots = 2048;
+
+__device__ __forceinline__ int32_t *dense_first(const RadixWs &ws) { return (int32_t *)ws.keyB; }
+__device__ __forceinline__ int32_t *dense_count(const RadixWs &ws, uint64_t nv) {
+  return (int32_t *)ws.keyB + nv;
+}
+
+__global__ void dense_clear_kernel(RadixWs ws) {
+  const uint64_t nv = ws.range[2];
+  if (!nv) return;
+  int32_t *first = dense_first(ws), *count = dense_count(ws, nv);
+  for (uint64_t v = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; v < nv;
+       v += (uint64_t)gridDim.x * blockDim.x) {
+    first[v] = 0x7fffffff;
+    count[v] = 0;
+  }
+}
+
+// Rounds of kAggRound consecutive requests are first combined per key value
+// in an LDS table (a hot key appears many times per round), then each table
+// entry goes to the value arrays with one atomic min and one atomic add.
+__global__ __launch_bounds__(256) void dense_mark_kernel(int R, RadixWs ws) {
+  __shared__ int32_t tkey[kAggSlots];
+  __shared__ int32_t tfirst[kAggSlots];
+  __shared__ int32_t tcount[kAggSlots];
+  const uint64_t nv = ws.range[2];
+  if (!nv) return;
+  const uint64_t mn = ws.range[0];
+  int32_t *first = dense_first(ws), *count = dense_count(ws, nv);
+  const int tid = threadIdx.x;
+  for (int r0 = blockIdx.x * kAggRound; r0 < R; r0 += gridDim.x * kAggRound) {
+    for (int j = tid; j < kAggSlots; j += 256) {
+      tkey[j] = -1;
+      tfirst[j] = 0x7fffffff;
+      tcount[j] = 0;
+    }
+    __syncthreads();
+    for (int j = tid; j < kAggRound; j += 256) {
+      const int p = r0 + j;
+      if (p >= R) break;
+      const int32_t v = (int32_t)(ws.keyA[p] - mn);   // < nv <= R
+      uint32_t h = ((uint32_t)v * 2654435761u) & (kAggSlots - 1);
+      for (;;) {   // at most kAggRound keys in kAggSlots slots: a slot is found
+        const int32_t prev = atomicCAS(&tkey[h], -1, v);
+        if (prev == -1 || prev == v) break;
+        h = (h + 1) & (kAggSlots - 1);
+      }
+      atomicMin(&tfirst[h], p);
+      atomicAdd(&tcount[h], 1);
+    }
+    __syncthreads();
+    for (int j = tid; j < kAggSlots; j += 256) {
+      const int32_t v = tkey[j];
+      if (v >= 0) {
+        atomicMin(&first[v], tfirst[j]);
+        atomicAdd(&count[v], tcount[j]);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// Present values per scan block.
+__global__ __launch_bounds__(kDenseBlk) void dense_blocksum_kernel(RadixWs ws) {
+  __shared__ uint32_t wsum[kDenseBlk / 64 + 1];
+  const uint64_t nv = ws.range[2];
+  if (!nv || (uint64_t)blockIdx.x * kDenseBlk >= nv) return;
+  const int32_t *count = dense_count(ws, nv);
+  const uint64_t v = (uint64_t)blockIdx.x * kDenseBlk + threadIdx.x;
+  const uint32_t pr = v < nv && count[v] > 0 ? 1u : 0u;
+  uint32_t total;
+  block_inclusive_scan<kDenseBlk>(pr, wsum, total);
+  if (threadIdx.x == 0) ws.hist[blockIdx.x] = total;
+}
+
+// Group numbers of the present values (ascending), and the per-group outputs.
+__global__ __launch_bounds__(kDenseBlk) void dense_groups_kernel(
+    RadixWs ws, int64_t *__restrict__ uk, int32_t *__restrict__ fi, int32_t *__restrict__ cnt,
+    int64_t *__restrict__ nu_out) {
+  __shared__ uint32_t wsum[kDenseBlk / 64 + 1];
+  const uint64_t nv = ws.range[2];
+  if (!nv || (uint64_t)blockIdx.x * kDenseBlk >= nv) return;
+  const uint64_t mn = ws.range[0];
+  const int32_t *first = dense_first(ws), *count = dense_count(ws, nv);
+  int32_t *gid = ws.idxB;
+  const int b = blockIdx.x, tid = threadIdx.x;
+  uint32_t before = 0;   // present values in all earlier blocks
+  for (int bb = tid; bb < b; bb += kDenseBlk) before += ws.hist[bb];
+  uint32_t g0;
+  block_inclusive_scan<kDenseBlk>(before, wsum, g0);
+  const uint64_t v = (uint64_t)b * kDenseBlk + tid;
+  const uint32_t pr = v < nv && count[v] > 0 ? 1u : 0u;
+  uint32_t total;
+  const uint32_t incl = block_inclusive_scan<kDenseBlk>(pr, wsum, total);
+  if (pr) {
+    const uint32_t g = g0 + incl - 1u;
+    uk[g] = unmap_key(mn + v);
+    fi[g] = first[v];
+    if (cnt) cnt[g] = count[v];
+    gid[v] = (int32_t)g;
+  }
+  if ((uint64_t)(b + 1) * kDenseBlk >= nv && tid == 0) *nu_out = (int64_t)(g0 + total);
+}
+
+__global__ void dense_inverse_kernel(int R, RadixWs ws, int32_t *__restrict__ inv) {
+  const uint64_t nv = ws.range[2];
+  if (!nv) return;
+  const uint64_t mn = ws.range[0];
+  for (int p = blockIdx.x * blockDim.x + threadIdx.x; p < R; p += gridDim.x * blockDim.x)
+    inv[p] = ws.idxB[ws.keyA[p] - mn];
 }
 
 // ---------------------------------------------------------------- host side
@@ -504,7 +635,7 @@ size_t dedup_workspace_bytes(int64_t R) {
   s += 2 * align_up(sizeof(uint64_t) * R);
   s += 2 * align_up(sizeof(int32_t) * R);
   s += 2 * align_up(sizeof(uint64_t) * nb);
-  s += align_up(sizeof(uint64_t) * 2);
+  s += align_up(sizeof(uint64_t) * 4);
   s += align_up(sizeof(uint32_t) * kBins * nb);
   s += align_up(sizeof(uint32_t) * nb);
   s += align_up(sizeof(int32_t) * (R + 1));
@@ -535,12 +666,23 @@ hipError_t launch_dedup(const int64_t *keys, int64_t R, int64_t *uk, int32_t *fi
   w.idxB = (int32_t *)p; p += align_up(sizeof(int32_t) * R);
   w.pmin = (uint64_t *)p; p += align_up(sizeof(uint64_t) * nb);
   w.pmax = (uint64_t *)p; p += align_up(sizeof(uint64_t) * nb);
-  w.range = (uint64_t *)p; p += align_up(sizeof(uint64_t) * 2);
+  w.range = (uint64_t *)p; p += align_up(sizeof(uint64_t) * 4);
   w.hist = (uint32_t *)p; p += align_up(sizeof(uint32_t) * kBins * nb);
   w.bheads = (uint32_t *)p; p += align_up(sizeof(uint32_t) * nb);
   w.start = (int32_t *)p;
   hipLaunchKernelGGL(radix_prep_kernel, dim3(nb), dim3(kRadixThreads), 0, st, keys, (int)R, w);
-  hipLaunchKernelGGL(radix_range_kernel, dim3(1), dim3(1024), 0, st, nb, w);
+  hipLaunchKernelGGL(radix_range_kernel, dim3(1), dim3(1024), 0, st, (int)R, nb, w);
+  // dense path (each kernel returns at once when the keys need the sort)
+  {
+    const unsigned vb = (unsigned)((R + kDenseBlk - 1) / kDenseBlk);   // nv <= R
+    hipLaunchKernelGGL(dense_clear_kernel, dim3(vb), dim3(kDenseBlk), 0, st, w);
+    hipLaunchKernelGGL(dense_mark_kernel, dim3((unsigned)((R + kAggRound - 1) / kAggRound)),
+                       dim3(256), 0, st, (int)R, w);
+    hipLaunchKernelGGL(dense_blocksum_kernel, dim3(vb), dim3(kDenseBlk), 0, st, w);
+    hipLaunchKernelGGL(dense_groups_kernel, dim3(vb), dim3(kDenseBlk), 0, st, w, uk, fi, cnt, nu);
+    hipLaunchKernelGGL(dense_inverse_kernel, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, st,
+                       (int)R, w, inv);
+  }
   for (int pass = 0; pass < 64 / kRadixBits; ++pass) {
     hipLaunchKernelGGL(radix_hist_kernel, dim3(nb), dim3(kRadixThreads), 0, st, (int)R, nb,
                        pass, w);

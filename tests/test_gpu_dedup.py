@@ -55,7 +55,9 @@ def test_dedup_workload_keys(name):
                                   "extremes_radix", "negative", "boundary_4096",
                                   "boundary_4097", "ragged_radix", "narrow_range_radix",
                                   "wide_and_narrow", "all_min_hash", "distinct_hash",
-                                  "boundary_2048", "boundary_2049", "high_bits_hash"])
+                                  "boundary_2048", "boundary_2049", "high_bits_hash",
+                                  "dense_span_r_minus_1", "radix_span_r", "dense_negative",
+                                  "dense_hot_zipf"])
 def test_dedup_edge_cases(case):
     # paths: hash table up to 2,048 keys, bitonic sort up to 4,096, radix sort
     rng = np.random.default_rng(zlib.crc32(case.encode()))
@@ -94,6 +96,16 @@ def test_dedup_edge_cases(case):
         keys = (rng.integers(0, 4096, size=1500).astype(np.int64) << 52)
     elif case == "ragged_radix":
         keys = rng.integers(-2 ** 40, 2 ** 40, size=3 * 4096 + 77).astype(np.int64)
+    elif case == "dense_span_r_minus_1":      # R values exactly: direct addressing
+        keys = (rng.permutation(9000) + 777).astype(np.int64)
+    elif case == "radix_span_r":              # one value more than R: the sort
+        keys = (rng.permutation(9001)[:9000] + 777).astype(np.int64)
+        keys[0], keys[1] = 777, 777 + 9000
+    elif case == "dense_negative":            # a narrow span around zero
+        keys = rng.integers(-3000, 3000, size=20_000).astype(np.int64)
+    elif case == "dense_hot_zipf":            # one key in half the requests
+        keys = rng.integers(0, 50_000, size=100_000).astype(np.int64)
+        keys[rng.random(100_000) < 0.5] = 31_337
     elif case == "narrow_range_radix":        # 18-bit span, far from zero
         keys = (rng.integers(0, 200_000, size=100_000) + 2 ** 50).astype(np.int64)
     else:                                     # one outlier forces all 64 bits
