@@ -22,8 +22,9 @@
  *                  Eq. 2; top-K vector retrieval of the RAG workloads, Sec. 4.1)
  *                  = hs_score_partial followed by hs_topk_merge.
  * Optionally, hs_cache_lookup / hs_cache_insert reuse results across windows
- * (Sec. 3.3 (II)), so that only keys not seen before are scored, and
- * hs_signature computes the keys themselves from node descriptions (Eq. 2).
+ * (Sec. 3.3 (II)), so that only keys not seen before are scored,
+ * hs_signature computes the keys themselves from node descriptions (Eq. 2),
+ * and hs_priority ranks the fused nodes for the ready queue (Eq. 3, Eq. 7).
  *
  * Conventions (all entry points):
  *   - Every function returns hs_status.  Arguments are validated on the host
