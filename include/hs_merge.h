@@ -73,7 +73,8 @@ typedef enum {
 
 /* Shape of one merge window (one call sequence). */
 typedef struct {
-    int64_t n_requests;   /* R >= 0: retrieval nodes in the window, arrival order */
+    int64_t n_requests;   /* R, 0 <= R <= 2^30: retrieval nodes in the window, in
+                             arrival order */
     int64_t dim;          /* d: vector width; F32: d % 4 == 0, BF16: d % 8 == 0,
                              FP8 corpus: d % 16 == 0; 1 <= d <= 16384 */
     int64_t n_corpus;     /* N: corpus rows, 0 <= N <= 2^31 - 1 */

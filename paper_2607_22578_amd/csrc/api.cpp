@@ -106,8 +106,10 @@ hs_status hs_merge_plan(const hs_merge_desc *desc, hs_plan **plan, size_t *works
     return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: null argument");
   const hs_merge_desc &d = *desc;
   if (d.flags != 0) return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: flags must be 0");
-  if (d.n_requests < 0 || d.n_requests > INT32_MAX)
-    return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: n_requests %lld out of [0, 2^31-1]",
+  // (2^30 keeps every request index and tile offset of the kernels' int32
+  // arithmetic far from overflow)
+  if (d.n_requests < 0 || d.n_requests > ((int64_t)1 << 30))
+    return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: n_requests %lld out of [0, 2^30]",
                 (long long)d.n_requests);
   if (d.n_corpus < 0 || d.n_corpus > INT32_MAX)
     return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: n_corpus %lld out of [0, 2^31-1]",

@@ -542,7 +542,8 @@ __global__ __launch_bounds__(256) void dense_mark_kernel(int R, RadixWs ws) {
   const uint64_t mn = ws.range[0];
   int32_t *first = dense_first(ws), *count = dense_count(ws, nv);
   const int tid = threadIdx.x;
-  for (int r0 = blockIdx.x * kAggRound; r0 < R; r0 += gridDim.x * kAggRound) {
+  for (int64_t r0 = (int64_t)blockIdx.x * kAggRound; r0 < R;
+       r0 += (int64_t)gridDim.x * kAggRound) {
     for (int j = tid; j < kAggSlots; j += 256) {
       tkey[j] = -1;
       tfirst[j] = 0x7fffffff;
@@ -550,7 +551,7 @@ __global__ __launch_bounds__(256) void dense_mark_kernel(int R, RadixWs ws) {
     }
     __syncthreads();
     for (int j = tid; j < kAggRound; j += 256) {
-      const int p = r0 + j;
+      const int64_t p = r0 + j;
       if (p >= R) break;
       const int32_t v = (int32_t)(ws.keyA[p] - mn);   // < nv <= R
       uint32_t h = ((uint32_t)v * 2654435761u) & (kAggSlots - 1);
@@ -559,7 +560,7 @@ __global__ __launch_bounds__(256) void dense_mark_kernel(int R, RadixWs ws) {
         if (prev == -1 || prev == v) break;
         h = (h + 1) & (kAggSlots - 1);
       }
-      atomicMin(&tfirst[h], p);
+      atomicMin(&tfirst[h], (int32_t)p);
       atomicAdd(&tcount[h], 1);
     }
     __syncthreads();
@@ -620,7 +621,8 @@ __global__ void dense_inverse_kernel(int R, RadixWs ws, int32_t *__restrict__ in
   const uint64_t nv = ws.range[2];
   if (!nv) return;
   const uint64_t mn = ws.range[0];
-  for (int p = blockIdx.x * blockDim.x + threadIdx.x; p < R; p += gridDim.x * blockDim.x)
+  for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < R;
+       p += (int64_t)gridDim.x * blockDim.x)
     inv[p] = ws.idxB[ws.keyA[p] - mn];
 }
 

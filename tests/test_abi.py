@@ -54,6 +54,7 @@ def test_plan_ok_and_workspace():
     (dict(dim=776, corpus_dtype=hs.HS_FP8_E4M3), hs.HS_ERR_UNSUPPORTED),  # fp8 needs d % 16
     (dict(n_requests=-1), hs.HS_ERR_INVALID_ARG),
     (dict(n_requests=2 ** 31), hs.HS_ERR_INVALID_ARG),
+    (dict(n_requests=2 ** 30 + 1), hs.HS_ERR_INVALID_ARG),
     (dict(n_corpus=-5), hs.HS_ERR_INVALID_ARG),
     (dict(n_corpus=2 ** 31), hs.HS_ERR_INVALID_ARG),
     (dict(query_dtype=7), hs.HS_ERR_UNSUPPORTED),
