@@ -19,10 +19,11 @@ pytestmark = pytest.mark.gpu
 N_CORPUS = 12_000     # 31 full 384-row tiles and a ragged one
 
 
-def _run(capacity, n_windows, k=10, enc="bf16", n_corpus=N_CORPUS):
+def _run(capacity, n_windows, k=10, enc="bf16", n_corpus=N_CORPUS, workload="ridge1m",
+         n_check=None):
     import paper_2607_22578_amd as hs
     dev = device()
-    wins = synth.window_stream("ridge1m", n_windows)
+    wins = synth.window_stream(workload, n_windows)
     d = wins[0].dim
     c, sc = synth.gaussian_rows(wins[0].seed, synth.S_CORPUS, n_corpus, d, enc)
     R = wins[0].R
@@ -56,7 +57,11 @@ def _run(capacity, n_windows, k=10, enc="bf16", n_corpus=N_CORPUS):
             np.testing.assert_array_equal(ti[u], i0)
         for u in np.nonzero(mp_ref >= 0)[0]:
             last[int(uk[u])] = (ts[u].copy(), ti[u].copy())
-        check_unique_topk(m, ref, win.q_req, c, k, scale=sc)
+        sel = None
+        if n_check is not None:   # a seeded sample of hits and misses
+            rng = np.random.default_rng(w)
+            sel = np.sort(rng.choice(nu, size=min(n_check, nu), replace=False))
+        check_unique_topk(m, ref, win.q_req, c, k, scale=sc, sel=sel)
         check_delivery(m, R)
         model.insert(uk, mp_ref, list(ts), list(ti))
         n_hits.append(int((mp_ref < 0).sum()))
@@ -143,3 +148,11 @@ def test_repeated_window_all_hits():
     assert (m.miss_pos[:nu] == -1).all()
     assert torch.equal(m.out_index, i1)
     assert torch.equal(m.out_score.view(torch.int32), s1.view(torch.int32))
+
+
+def test_many_distinct_keys():
+    # 32,768 requests per window (~10k distinct): the store's multi-workgroup
+    # insert path, k = 32
+    hits = _run(16384, 2, k=32, n_corpus=3000, workload="mfma4m", n_check=64)
+    assert hits[0] == 0 and hits[1] > 0
+
