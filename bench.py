@@ -32,6 +32,7 @@ sys.path.insert(0, ROOT)
 METRIC = "merged retrieval queries/s + achieved HBM GB/s or MFMA % (dedup+score+top-k)"
 PEAK_HBM_GBS = 8000.0
 PEAK_MFMA = {"bf16": 2500.0}          # dense TFLOP/s (no sparsity)
+PEAK_FP32_VECTOR = 157.3              # TFLOP/s, fp32 on the vector units
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_step_ridge1m_traffic.json")
 KERNEL_SOURCES = ["paper_2607_22578_amd/csrc/score_mfma.hip", "paper_2607_22578_amd/csrc/score.hip",
                   "paper_2607_22578_amd/csrc/common.h"]
@@ -70,7 +71,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="ridge1m",
-                    help="ridge1m (default), mfma4m or fp8_20m")
+                    help="ridge1m (default), mfma4m, fp8_20m, tiny or dedup256k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=96,
                     help="distinct queries scored by the oracle for the CPU baseline")
@@ -153,8 +154,9 @@ def main():
         w.keys = np.arange(w.R, dtype=np.int64)
     cfg = w.cfg
     R, d, N, k = w.R, w.dim, w.n_corpus, w.k
-    qdt = hs.HS_BF16
-    cdt = {"bf16": hs.HS_BF16, "fp8": hs.HS_FP8_E4M3}[cfg.c_enc]
+    enc = {"f32": hs.HS_F32, "bf16": hs.HS_BF16, "fp8": hs.HS_FP8_E4M3}
+    qdt, cdt = enc[cfg.q_enc], enc[cfg.c_enc]
+    f32 = cfg.c_enc == "f32"
 
     def to_dev(a):
         if a.dtype == np.uint16:
@@ -299,8 +301,9 @@ def main():
                       (acc / max(reps, 1)).round(4).tolist())) if reps else None
 
     # roofline of the scoring kernel: algorithmic work per launch
-    c_bytes = N * d * (1 if cfg.c_enc == "fp8" else 2) + (N * 4 if cfg.c_enc == "fp8" else 0)
-    q_bytes = n_u * d * 2
+    c_bytes = N * d * {"fp8": 1, "bf16": 2, "f32": 4}[cfg.c_enc] + \
+        (N * 4 if cfg.c_enc == "fp8" else 0)
+    q_bytes = n_u * d * (4 if f32 else 2)
     alg_bytes = c_bytes + q_bytes
     alg_flops = 2.0 * n_u * N * d
     t_s = kern_ms * 1e-3
@@ -308,7 +311,14 @@ def main():
     gbs = alg_bytes / t_s / 1e9
     t_mfma = alg_flops / (PEAK_MFMA["bf16"] * 1e12)
     t_hbm = alg_bytes / (PEAK_HBM_GBS * 1e9)
-    if t_mfma >= t_hbm:
+    t_alu = alg_flops / (PEAK_FP32_VECTOR * 1e12)
+    if f32 and t_alu >= t_hbm:   # fp32 inputs run on the vector units
+        roof = {"bound": "alu", "achieved": round(tflops, 3), "peak": PEAK_FP32_VECTOR,
+                "unit": "TFLOP/s", "frac": round(tflops / PEAK_FP32_VECTOR, 4)}
+    elif f32:
+        roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    elif t_mfma >= t_hbm:
         roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_MFMA["bf16"],
                 "unit": "TFLOP/s", "frac": round(tflops / PEAK_MFMA["bf16"], 4)}
     else:
@@ -337,8 +347,8 @@ def main():
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "queries/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
-        "data": "synthetic",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32" if f32 else "bf16", "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {cfg.desc}", "n_requests": R, "n_unique": n_distinct,
                    "dim": d, "n_corpus": N, "k": k, "query_dtype": cfg.q_enc,
                    "corpus_dtype": cfg.c_enc, "seed": w.seed,
