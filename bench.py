@@ -42,6 +42,7 @@ KERNEL_SOURCES = ["paper_2607_22578_amd/csrc/score_mfma.hip", "paper_2607_22578_
 EV_EVERY = 4
 SCORE_STEP = ("score step = score_mfma_dma (seed pass) + mfma_seed_kernel + "
               "score_mfma_dma (main pass)")
+SCORE_STEP_VALU = "score step = score_partial_valu (fp32, vector units)"
 
 
 DEDUP_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dedup_gather_dedup256k_traffic.json")
@@ -325,7 +326,7 @@ def main():
         roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
     roof["traffic"] = None
-    roof["kernel"] = SCORE_STEP
+    roof["kernel"] = SCORE_STEP_VALU if f32 else SCORE_STEP
     roof["kernel_ms"] = round(kern_ms, 4)
     roof["kernel_ms_p10_p50_p90"] = [round(float(np.percentile(kern_samples, p)), 4)
                                      for p in (10, 50, 90)]

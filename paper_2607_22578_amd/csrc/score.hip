@@ -11,8 +11,10 @@
 // turns out to be.  bf16 and fp8 corpora run on the matrix cores
 // (score_mfma.hip); fp32 inputs run score_partial_valu below: plain VALU FMA
 // tiles through LDS, then each query with a possible entrant has its tile row
-// scanned by one thread that keeps the query's k best (score, row) keys of
-// this slice.
+// merged into the query's k best (score, row) keys of this slice: by one
+// wave that ranks the tile's keys and the list's together (k <= 32: the list
+// lives in LDS and stays sorted), else by one thread that replaces the list's
+// minimum key by key.
 // Phase 2 (topk_merge_kernel): per query, the S slice lists (S*k keys) are
 // filtered (empty keys, and keys below the query's shared threshold on the
 // matrix-core path), the rest sorted and the first k written out.
@@ -126,6 +128,62 @@ __device__ void scan_tile(const TileState &ts, const ScoreArgs &a, const float *
   ts.thr[q] = mn ? unord_score((uint32_t)(mn >> 32)) : -__builtin_inff();
 }
 
+// LDS lists (k <= kListLdsMaxK): one wave per flagged query.  Lane i holds
+// the key of tile row i (0 past the corpus end); every key of the union of
+// those NC keys and the query's k list keys is ranked by counting the larger
+// ones (keys are distinct, except the empty key 0), and the nonzero keys
+// ranked below k are written to their rank.  The list thus stays sorted in
+// descending order, positions past its nonzero keys keep 0, and the key of
+// rank k-1 is its new minimum.  u is this wave's [NC + kListLdsMaxK] scratch.
+template <int MQ, int NC, int LD>
+__device__ void scan_tile_wave(const TileState &ts, const ScoreArgs &a, const float *dump,
+                               uint64_t *u, int64_t qbase, int64_t nu, int64_t rbase) {
+  static_assert(NC == kWave, "one tile row per lane");
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
+  const int nw = blockDim.x / kWave;
+  const int k = a.k;
+  const int64_t nvalid = a.N - rbase < NC ? a.N - rbase : NC;
+  for (int q = wave; q < MQ; q += nw) {
+    if (qbase + q >= nu || !ts.flag[q]) continue;
+    uint64_t *l = ts.lists + (int64_t)q * k;
+    const uint64_t x0 = lane < nvalid ? make_key(dump[q * LD + lane], (uint32_t)(rbase + lane))
+                                      : 0ull;
+    const uint64_t x1 = lane < k ? l[lane] : 0ull;
+    u[lane] = x0;
+    if (lane < kListLdsMaxK) u[NC + lane] = x1;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    int r0 = 0, r1 = 0;
+    for (int j = 0; j < NC + kListLdsMaxK; j += 8) {
+      uint64_t b[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) b[t] = u[j + t];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        r0 += b[t] > x0 ? 1 : 0;
+        r1 += b[t] > x1 ? 1 : 0;
+      }
+    }
+    if (x0 != 0ull && r0 < k) l[r0] = x0;
+    if (x1 != 0ull && r1 < k) l[r1] = x1;
+    if (x0 != 0ull && r0 == k - 1) {
+      ts.lmin[q] = x0;
+      ts.thr[q] = unord_score((uint32_t)(x0 >> 32));
+    }
+    if (x1 != 0ull && r1 == k - 1) {
+      ts.lmin[q] = x1;
+      ts.thr[q] = unord_score((uint32_t)(x1 >> 32));
+    }
+    if (lane == 0) ts.flag[q] = 0;
+    // the scratch is rewritten for the next query only after every lane
+    // has read it
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+
 template <int MQ>
 __device__ void flush_lists(const TileState &ts, const ScoreArgs &a, int64_t qbase, int64_t nu,
                             int64_t S, int64_t s) {
@@ -143,7 +201,8 @@ __device__ void flush_lists(const TileState &ts, const ScoreArgs &a, int64_t qba
 __host__ __device__ constexpr int valu_lds_bytes(bool lds_lists, int k) {
   return (2 * kVNC * kVLd * 4 > kVMQ * kVDumpLd * 4 ? 2 * kVNC * kVLd * 4
                                                     : kVMQ * kVDumpLd * 4) +
-         kVMQ * (8 + 4 + 4 + 4) + (lds_lists ? kVMQ * k * 8 : 0);
+         kVMQ * (8 + 4 + 4 + 4) +
+         (lds_lists ? kVMQ * k * 8 + kThreads / kWave * (kVNC + kListLdsMaxK) * 8 : 0);
 }
 
 // 16 x 16 threads; thread (ty, tx) computes queries 4*ty.. x rows 4*tx.. .
@@ -162,6 +221,9 @@ __global__ __launch_bounds__(kThreads) void score_partial_valu(ScoreArgs a) {
   ts.thr = reinterpret_cast<float *>(p); p += kVMQ * 4;
   ts.flag = reinterpret_cast<int32_t *>(p); p += kVMQ * 4;
   ts.lists = LDS_LISTS ? reinterpret_cast<uint64_t *>(p) : nullptr;
+  uint64_t *wave_u = LDS_LISTS ? reinterpret_cast<uint64_t *>(p) + kVMQ * a.k +
+                                     (threadIdx.x / kWave) * (kVNC + kListLdsMaxK)
+                               : nullptr;
 
   const int64_t nu = read_nu(a.n_unique, a.n_unique_dev, a.cap);
   const Split sp = split_for(nu, a.N, kVMQ, kVNC, a.grid, a.k);
@@ -217,7 +279,10 @@ __global__ __launch_bounds__(kThreads) void score_partial_valu(ScoreArgs a) {
             make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
       }
       __syncthreads();
-      scan_tile<kVMQ, kVNC, kVDumpLd>(ts, a, dump, qbase, nu, rbase, sp.S, s);
+      if (LDS_LISTS)
+        scan_tile_wave<kVMQ, kVNC, kVDumpLd>(ts, a, dump, wave_u, qbase, nu, rbase);
+      else
+        scan_tile<kVMQ, kVNC, kVDumpLd>(ts, a, dump, qbase, nu, rbase, sp.S, s);
       __syncthreads();
     }
     flush_lists<kVMQ>(ts, a, qbase, nu, sp.S, s);
@@ -453,7 +518,7 @@ hipError_t launch_topk_merge(const void *part, int64_t n_unique, const int64_t *
   if (blocks > 2 * (int64_t)grid) blocks = 2 * (int64_t)grid;
   hipLaunchKernelGGL(topk_merge_kernel, dim3((unsigned)blocks), dim3(kMergeThreads), 0, st,
                      (const uint64_t *)part, thr, n_unique, nu_dev, cap, N, k, mq, nc, smax, grid,
-                     valu ? 0 : 1, out_s, out_i);
+                     valu && k > kListLdsMaxK ? 0 : 1, out_s, out_i);
   return hipGetLastError();
 }
 
