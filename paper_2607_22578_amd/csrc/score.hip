@@ -205,7 +205,29 @@ __host__ __device__ constexpr int valu_lds_bytes(bool lds_lists, int k) {
          (lds_lists ? kVMQ * k * 8 + kThreads / kWave * (kVNC + kListLdsMaxK) * 8 : 0);
 }
 
-// 16 x 16 threads; thread (ty, tx) computes queries 4*ty.. x rows 4*tx.. .
+// One K chunk of a thread's register tile: NI of its queries (ty + 16 i,
+// i < NI) by its four rows 4 tx + j.
+template <int NI>
+__device__ __forceinline__ void valu_chunk(float (&acc)[4][4], const float *Qs, const float *Cs,
+                                           int ty, int tx) {
+  for (int c = 0; c < kVKC; ++c) {
+    float qv[NI], cv[4];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) qv[i] = Qs[(ty + 16 * i) * kVLd + c];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cv[j] = Cs[(4 * tx + j) * kVLd + c];
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(qv[i], cv[j], acc[i][j]);
+  }
+}
+
+// 16 x 16 threads; thread (ty, tx) computes queries ty + 16 i (i < 4) x rows
+// 4 tx + j (j < 4).  Queries are interleaved over the waves (wave w holds
+// ty = 4w .. 4w+3), so a tile with few live queries spreads them over all
+// four SIMDs, and each wave multiplies only the query rows i that are live
+// for one of its lanes (a wave-uniform count).
 template <bool LDS_LISTS>
 __global__ __launch_bounds__(kThreads) void score_partial_valu(ScoreArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -236,6 +258,9 @@ __global__ __launch_bounds__(kThreads) void score_partial_valu(ScoreArgs a) {
     const int64_t qt = w % sp.qtiles, s = w / sp.qtiles;
     const int64_t t0 = s * sp.ntiles / sp.S, t1 = (s + 1) * sp.ntiles / sp.S;
     const int64_t qbase = qt * kVMQ;
+    const int64_t live = nu - qbase;   // >= 1
+    const int lo = 4 * (tid >> 6);     // smallest ty of this wave
+    const int ni = live <= lo ? 0 : (live - lo + 15) / 16 > 4 ? 4 : (int)((live - lo + 15) / 16);
     init_lists<kVMQ>(ts, a, qbase, nu, sp.S, s);
     __syncthreads();
     for (int64_t t = t0; t < t1; ++t) {
@@ -254,22 +279,18 @@ __global__ __launch_bounds__(kThreads) void score_partial_valu(ScoreArgs a) {
           Qs[r * kVLd + c] = (gq < nu && gc < a.d) ? Q[gq * a.d + gc] : 0.0f;
         }
         __syncthreads();
-        for (int c = 0; c < kVKC; ++c) {
-          float qv[4], cv[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) qv[i] = Qs[(4 * ty + i) * kVLd + c];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) cv[j] = Cs[(4 * tx + j) * kVLd + c];
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(qv[i], cv[j], acc[i][j]);
+        switch (ni) {
+          case 4: valu_chunk<4>(acc, Qs, Cs, ty, tx); break;
+          case 3: valu_chunk<3>(acc, Qs, Cs, ty, tx); break;
+          case 2: valu_chunk<2>(acc, Qs, Cs, ty, tx); break;
+          case 1: valu_chunk<1>(acc, Qs, Cs, ty, tx); break;
+          default: break;
         }
         __syncthreads();
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int q = 4 * ty + i;
+        const int q = ty + 16 * i;
         const float th = ts.thr[q];
         bool hit = false;
 #pragma unroll

@@ -49,6 +49,22 @@ def test_fp32_multi_query_tiles_ragged():
     check_delivery(m, cfg_w.R)
 
 
+@pytest.mark.parametrize("k", [1, 32, 33, 100])
+def test_fp32_k_values(k):
+    # k <= 32: lists in LDS merged by one wave per query (sorted lists);
+    # k > 32: lists in the workspace, one thread per query; 329 distinct
+    # queries over 5,003 rows (6 query tiles, the last with 9 live queries)
+    cfg_w = synth.make("ridge1m", n_corpus=5_003, with_corpus=False)
+    q, _ = synth.gaussian_rows(cfg_w.seed, synth.S_QUERY, 0, 384, "f32",
+                               row_ids=cfg_w.template_ids)
+    c, _ = synth.gaussian_rows(cfg_w.seed, synth.S_CORPUS, 5_003, 384, "f32")
+    note(f"fp32 k={k}")
+    m = run_merge(cfg_w.keys, q, c, k)
+    ref = check_dedup(m, cfg_w.keys)
+    check_unique_topk(m, ref, q, c, k)
+    check_delivery(m, cfg_w.R)
+
+
 @pytest.mark.parametrize("k", [1, 32, 100])
 def test_k_values(k):
     w = synth.make("ridge1m", n_corpus=9_000)
