@@ -205,6 +205,24 @@ __host__ __device__ constexpr int valu_lds_bytes(bool lds_lists, int k) {
          (lds_lists ? kVMQ * k * 8 + kThreads / kWave * (kVNC + kListLdsMaxK) * 8 : 0);
 }
 
+constexpr int kVLoads = kVNC * kVKC / kThreads;   // corpus (and query) floats per thread
+static_assert(kVNC == kVMQ && kVLoads * kThreads == kVNC * kVKC, "chunk split");
+
+// A thread's share of K chunk kc: corpus rows rbase + r and query rows
+// qbase + r, columns kc + c, 0 past the corpus, the live queries or d.
+__device__ __forceinline__ void valu_fetch(float (&cr)[kVLoads], float (&qr)[kVLoads],
+                                           const float *C, const float *Q, const ScoreArgs &a,
+                                           int64_t rbase, int64_t qbase, int64_t nu, int64_t kc,
+                                           int tid) {
+#pragma unroll
+  for (int u = 0; u < kVLoads; ++u) {
+    const int e = tid + u * kThreads, r = e / kVKC, c = e % kVKC;
+    const int64_t gr = rbase + r, gc = kc + c, gq = qbase + r;
+    cr[u] = (gr < a.N && gc < a.d) ? C[gr * a.d + gc] : 0.0f;
+    qr[u] = (gq < nu && gc < a.d) ? Q[gq * a.d + gc] : 0.0f;
+  }
+}
+
 // One K chunk of a thread's register tile: NI of its queries (ty + 16 i,
 // i < NI) by its four rows 4 tx + j.
 template <int NI>
@@ -270,15 +288,19 @@ __global__ __launch_bounds__(kThreads) void score_partial_valu(ScoreArgs a) {
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = 0.0f;
+      // the next K chunk is loaded into registers while this one is
+      // multiplied, so its memory latency overlaps the FMAs
+      float cr[kVLoads], qr[kVLoads];
+      valu_fetch(cr, qr, C, Q, a, rbase, qbase, nu, 0, tid);
       for (int64_t kc = 0; kc < a.d; kc += kVKC) {
-        for (int e = tid; e < kVNC * kVKC; e += kThreads) {
-          int r = e / kVKC, c = e % kVKC;
-          int64_t gr = rbase + r, gc = kc + c;
-          Cs[r * kVLd + c] = (gr < a.N && gc < a.d) ? C[gr * a.d + gc] : 0.0f;
-          int64_t gq = qbase + r;
-          Qs[r * kVLd + c] = (gq < nu && gc < a.d) ? Q[gq * a.d + gc] : 0.0f;
+#pragma unroll
+        for (int u = 0; u < kVLoads; ++u) {
+          const int e = tid + u * kThreads, r = e / kVKC, c = e % kVKC;
+          Cs[r * kVLd + c] = cr[u];
+          Qs[r * kVLd + c] = qr[u];
         }
         __syncthreads();
+        if (kc + kVKC < a.d) valu_fetch(cr, qr, C, Q, a, rbase, qbase, nu, kc + kVKC, tid);
         switch (ni) {
           case 4: valu_chunk<4>(acc, Qs, Cs, ty, tx); break;
           case 3: valu_chunk<3>(acc, Qs, Cs, ty, tx); break;
