@@ -241,6 +241,28 @@ __device__ __forceinline__ void valu_chunk(float (&acc)[4][4], const float *Qs, 
   }
 }
 
+// Registers of valu_fetch into the LDS chunk.
+__device__ __forceinline__ void valu_stage(const float (&cr)[kVLoads], const float (&qr)[kVLoads],
+                                           float *Cs, float *Qs, int tid) {
+#pragma unroll
+  for (int u = 0; u < kVLoads; ++u) {
+    const int e = tid + u * kThreads, r = e / kVKC, c = e % kVKC;
+    Cs[r * kVLd + c] = cr[u];
+    Qs[r * kVLd + c] = qr[u];
+  }
+}
+
+__device__ __forceinline__ void valu_multiply(int ni, float (&acc)[4][4], const float *Qs,
+                                              const float *Cs, int ty, int tx) {
+  switch (ni) {
+    case 4: valu_chunk<4>(acc, Qs, Cs, ty, tx); break;
+    case 3: valu_chunk<3>(acc, Qs, Cs, ty, tx); break;
+    case 2: valu_chunk<2>(acc, Qs, Cs, ty, tx); break;
+    case 1: valu_chunk<1>(acc, Qs, Cs, ty, tx); break;
+    default: break;
+  }
+}
+
 // 16 x 16 threads; thread (ty, tx) computes queries ty + 16 i (i < 4) x rows
 // 4 tx + j (j < 4).  Queries are interleaved over the waves (wave w holds
 // ty = 4w .. 4w+3), so a tile with few live queries spreads them over all
@@ -288,26 +310,23 @@ __global__ __launch_bounds__(kThreads) void score_partial_valu(ScoreArgs a) {
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = 0.0f;
-      // the next K chunk is loaded into registers while this one is
-      // multiplied, so its memory latency overlaps the FMAs
-      float cr[kVLoads], qr[kVLoads];
-      valu_fetch(cr, qr, C, Q, a, rbase, qbase, nu, 0, tid);
-      for (int64_t kc = 0; kc < a.d; kc += kVKC) {
-#pragma unroll
-        for (int u = 0; u < kVLoads; ++u) {
-          const int e = tid + u * kThreads, r = e / kVKC, c = e % kVKC;
-          Cs[r * kVLd + c] = cr[u];
-          Qs[r * kVLd + c] = qr[u];
-        }
+      // K chunks are loaded into registers two ahead of the one being
+      // multiplied (two register sets in turn), so their memory latency
+      // overlaps the FMAs and the loads of the next chunk
+      float cr0[kVLoads], qr0[kVLoads], cr1[kVLoads], qr1[kVLoads];
+      valu_fetch(cr0, qr0, C, Q, a, rbase, qbase, nu, 0, tid);
+      if (kVKC < a.d) valu_fetch(cr1, qr1, C, Q, a, rbase, qbase, nu, kVKC, tid);
+      for (int64_t kc = 0; kc < a.d; kc += 2 * kVKC) {
+        valu_stage(cr0, qr0, Cs, Qs, tid);
         __syncthreads();
-        if (kc + kVKC < a.d) valu_fetch(cr, qr, C, Q, a, rbase, qbase, nu, kc + kVKC, tid);
-        switch (ni) {
-          case 4: valu_chunk<4>(acc, Qs, Cs, ty, tx); break;
-          case 3: valu_chunk<3>(acc, Qs, Cs, ty, tx); break;
-          case 2: valu_chunk<2>(acc, Qs, Cs, ty, tx); break;
-          case 1: valu_chunk<1>(acc, Qs, Cs, ty, tx); break;
-          default: break;
-        }
+        if (kc + 2 * kVKC < a.d) valu_fetch(cr0, qr0, C, Q, a, rbase, qbase, nu, kc + 2 * kVKC, tid);
+        valu_multiply(ni, acc, Qs, Cs, ty, tx);
+        __syncthreads();
+        if (kc + kVKC >= a.d) break;
+        valu_stage(cr1, qr1, Cs, Qs, tid);
+        __syncthreads();
+        if (kc + 3 * kVKC < a.d) valu_fetch(cr1, qr1, C, Q, a, rbase, qbase, nu, kc + 3 * kVKC, tid);
+        valu_multiply(ni, acc, Qs, Cs, ty, tx);
         __syncthreads();
       }
 #pragma unroll
