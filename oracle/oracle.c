@@ -177,58 +177,36 @@ static void list_insert(double *bs, int64_t *bi, int64_t kk, int64_t *filled, do
 }
 
 /* For each selected query row q_rows[t] (or t when q_rows is NULL), the kk
- * best corpus rows by (score desc, index asc).  Outputs [n_sel x kk]:
- * best_score (double, exact), best_index (int64); slots beyond N hold
- * (-inf, -1).  The corpus is cut into chunks so that few queries still use
- * every thread: each (query, chunk) keeps the kk best of its chunk, and the
- * chunk lists of a query are then merged with the same insertion -- the kk
- * best of a union are among the kk best of its parts. */
+ * best corpus rows by (score desc, index asc): one pass over all N corpus rows
+ * in index order, each exact score offered to a sorted kk-entry list.  Outputs
+ * [n_sel x kk]: best_score (double, exact), best_index (int64); slots beyond N
+ * hold (-inf, -1).  Queries are independent; threads split the queries only,
+ * so every list sees the rows exactly as in the definition. */
 int or_topk_exact(const void *Q, int q_enc, int64_t n_sel, const int64_t *q_rows,
                   const void *C, int c_enc, const float *scale, int64_t N, int64_t d,
                   int64_t kk, double *best_score, int64_t *best_index, int threads) {
     if (n_sel < 0 || N < 0 || d <= 0 || kk <= 0) return -1;
     if (threads < 1) threads = 1;
     init_tables();
-    int64_t nch = n_sel > 0 ? (threads + n_sel - 1) / n_sel : 1;
-    if (nch > 64) nch = 64;
-    if (nch > N) nch = N > 0 ? N : 1;
-    if (nch < 1) nch = 1;
-    int64_t per = (N + nch - 1) / nch;
-    size_t cells = (size_t)(n_sel > 0 ? n_sel : 1) * (size_t)nch * (size_t)kk;
-    double *cs = (double *)malloc(sizeof(double) * cells);
-    int64_t *ci = (int64_t *)malloc(sizeof(int64_t) * cells);
-    int64_t *cf = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n_sel > 0 ? n_sel : 1) * (size_t)nch);
-    if (!cs || !ci || !cf) { free(cs); free(ci); free(cf); return -1; }
     int err = 0;
 #pragma omp parallel for num_threads(threads) schedule(dynamic, 1)
-    for (int64_t w = 0; w < n_sel * nch; ++w) {
-        int64_t t = w / nch, ch = w % nch;
-        int64_t q = q_rows ? q_rows[t] : t;
-        double *bs = cs + w * kk;
-        int64_t *bi = ci + w * kk;
-        int64_t filled = 0;
-        double *qv = (double *)malloc(sizeof(double) * (size_t)d);
-        if (!qv) { err = -1; cf[w] = 0; continue; }
-        widen_row(Q, q_enc, q, d, qv);
-        int64_t c1 = (ch + 1) * per < N ? (ch + 1) * per : N;
-        for (int64_t c = ch * per; c < c1; ++c)
-            list_insert(bs, bi, kk, &filled, score_row(qv, C, c_enc, scale, c, d), c);
-        cf[w] = filled;
-        free(qv);
-    }
-#pragma omp parallel for num_threads(threads) schedule(static)
     for (int64_t t = 0; t < n_sel; ++t) {
+        int64_t q = q_rows ? q_rows[t] : t;
         double *bs = best_score + t * kk;
         int64_t *bi = best_index + t * kk;
         int64_t filled = 0;
-        for (int64_t ch = 0; ch < nch; ++ch) {
-            int64_t w = t * nch + ch;
-            for (int64_t j = 0; j < cf[w]; ++j)
-                list_insert(bs, bi, kk, &filled, cs[w * kk + j], ci[w * kk + j]);
+        double *qv = (double *)malloc(sizeof(double) * (size_t)d);
+        if (!qv) {
+#pragma omp atomic write
+            err = -1;
+            continue;
         }
+        widen_row(Q, q_enc, q, d, qv);
+        for (int64_t c = 0; c < N; ++c)
+            list_insert(bs, bi, kk, &filled, score_row(qv, C, c_enc, scale, c, d), c);
         for (int64_t j = filled; j < kk; ++j) { bs[j] = -INFINITY; bi[j] = -1; }
+        free(qv);
     }
-    free(cs); free(ci); free(cf);
     return err;
 }
 

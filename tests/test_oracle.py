@@ -167,14 +167,45 @@ def test_topk_matches_bruteforce(enc, seed):
         if sc is not None:
             sc[b] = sc[a]
     S, rs, ri = _brute(Q, C, kk, sc)
-    s, i = oracle.topk_exact(Q, C, kk, scale=sc)
-    np.testing.assert_array_equal(i, ri)
-    np.testing.assert_allclose(s, rs, rtol=1e-12, atol=1e-15)
+    for threads in (1, 3, 64):
+        s, i = oracle.topk_exact(Q, C, kk, scale=sc, threads=threads)
+        np.testing.assert_array_equal(i, ri)
+        np.testing.assert_allclose(s, rs, rtol=1e-12, atol=1e-15)
     # exact scores of explicit pairs agree with the library matmul
     qi = rng.integers(0, n, 50)
     ci = rng.integers(0, N, 50)
     np.testing.assert_allclose(oracle.score_pairs(Q, C, qi, ci, scale=sc), S[qi, ci],
                                rtol=1e-12, atol=1e-15)
+
+
+@pytest.mark.parametrize("threads", [1, 2, 64])
+def test_topk_ties_straddling_rank_k(threads):
+    # Groups of identical corpus rows whose scores tie exactly; one group is
+    # planted so that it straddles rank k (its lower rows must be kept, in
+    # ascending order), against the lexsort brute force.  Few queries and a
+    # small corpus, with any thread count.
+    d, N, kk = 16, 97, 7
+    C, _ = synth.gaussian_rows(12, 90, N, d, "bf16")
+    Q, _ = synth.gaussian_rows(12, 89, 3, d, "bf16")
+    S0 = _decode_np(Q) @ _decode_np(C).T
+    # the row ranked 5th for query 0 gets four copies spread over the corpus,
+    # so ranks 5..8 tie and rank k = 7 cuts the group
+    r5 = int(np.lexsort((np.arange(N), -S0[0]))[4])
+    for b in (3, 50, 90):
+        if b != r5:
+            C[b] = C[r5]
+    S, rs, ri = _brute(Q, C, kk)
+    s, i = oracle.topk_exact(Q, C, kk, threads=threads)
+    np.testing.assert_array_equal(i, ri)
+    np.testing.assert_array_equal(s, rs)
+    tied = sorted({r5, 3, 50, 90})
+    assert i[0, 4:7].tolist() == tied[:3]
+    assert s[0, 4] == s[0, 5] == s[0, 6]
+    # one query and a corpus smaller than the thread count
+    s1, i1 = oracle.topk_exact(Q[:1], C[:5], 9, threads=threads)
+    _, rs1, ri1 = _brute(Q[:1], C[:5], 9)
+    np.testing.assert_array_equal(i1, ri1)
+    assert np.all(i1[0, 5:] == -1) and np.all(np.isneginf(s1[0, 5:]))
 
 
 def test_unit_query_picks_column():
