@@ -59,12 +59,14 @@ double or_e4m3_decode(uint8_t code) {
 }
 
 /* bfloat16 is the upper half of an IEEE binary32. */
-double or_bf16_decode(uint16_t bits) {
+static double bf16_value(uint16_t bits) {
     uint32_t w = (uint32_t)bits << 16;
     float f;
     memcpy(&f, &w, 4);
     return (double)f;
 }
+
+double or_bf16_decode(uint16_t bits) { return bf16_value(bits); }
 
 /* The 256 E4M3 values, tabulated once from or_e4m3_decode. */
 static double e4m3_table[256];
@@ -74,14 +76,6 @@ static void init_tables(void) {
     if (e4m3_table_ready) return;
     for (int c = 0; c < 256; ++c) e4m3_table[c] = or_e4m3_decode((uint8_t)c);
     e4m3_table_ready = 1;
-}
-
-static double elem(const void *base, int enc, int64_t i) {
-    switch (enc) {
-    case OR_F32: return (double)((const float *)base)[i];
-    case OR_BF16: return or_bf16_decode(((const uint16_t *)base)[i]);
-    default: return e4m3_table[((const uint8_t *)base)[i]];
-    }
 }
 
 /* ---- step 1: deduplication ----------------------------------------------- */
@@ -142,18 +136,32 @@ int or_gather_rows(const void *src, int64_t src_rows, int64_t row_bytes,
 
 /* ---- steps 3 and 4: exact scores and top-k ------------------------------- */
 
-/* exact s(q, c) = scale_c * sum_j q[j] * C[c, j]  (scale_c = 1 unless fp8);
- * q is the query row already widened to double. */
-static double score_row(const double *q, const void *C, int c_enc,
-                        const float *scale, int64_t c, int64_t d) {
-    double acc = 0.0;
-    for (int64_t j = 0; j < d; ++j) acc += q[j] * elem(C, c_enc, c * d + j);
-    if (c_enc == OR_FP8) acc *= (double)scale[c];
-    return acc;
+/* Row r of a [rows x d] matrix in encoding enc, widened exactly to double. */
+static void widen_row(const void *M, int enc, int64_t r, int64_t d, double *out) {
+    const int64_t o = r * d;
+    switch (enc) {
+    case OR_F32:
+        for (int64_t j = 0; j < d; ++j) out[j] = (double)((const float *)M)[o + j];
+        break;
+    case OR_BF16:
+        for (int64_t j = 0; j < d; ++j) out[j] = bf16_value(((const uint16_t *)M)[o + j]);
+        break;
+    default:
+        for (int64_t j = 0; j < d; ++j) out[j] = e4m3_table[((const uint8_t *)M)[o + j]];
+        break;
+    }
 }
 
-static void widen_row(const void *Q, int q_enc, int64_t q, int64_t d, double *out) {
-    for (int64_t j = 0; j < d; ++j) out[j] = elem(Q, q_enc, q * d + j);
+/* exact s(q, c) = scale_c * sum_j q[j] * C[c, j]  (scale_c = 1 unless fp8);
+ * q is the query row already widened to double, crow is scratch for the
+ * widened corpus row. */
+static double score_row(const double *q, const void *C, int c_enc,
+                        const float *scale, int64_t c, int64_t d, double *crow) {
+    widen_row(C, c_enc, c, d, crow);
+    double acc = 0.0;
+    for (int64_t j = 0; j < d; ++j) acc += q[j] * crow[j];
+    if (c_enc == OR_FP8) acc *= (double)scale[c];
+    return acc;
 }
 
 /* (sa, ca) ranks before (sb, cb): higher score first, then lower index. */
@@ -195,7 +203,7 @@ int or_topk_exact(const void *Q, int q_enc, int64_t n_sel, const int64_t *q_rows
         double *bs = best_score + t * kk;
         int64_t *bi = best_index + t * kk;
         int64_t filled = 0;
-        double *qv = (double *)malloc(sizeof(double) * (size_t)d);
+        double *qv = (double *)malloc(sizeof(double) * 2 * (size_t)d);
         if (!qv) {
 #pragma omp atomic write
             err = -1;
@@ -203,7 +211,7 @@ int or_topk_exact(const void *Q, int q_enc, int64_t n_sel, const int64_t *q_rows
         }
         widen_row(Q, q_enc, q, d, qv);
         for (int64_t c = 0; c < N; ++c)
-            list_insert(bs, bi, kk, &filled, score_row(qv, C, c_enc, scale, c, d), c);
+            list_insert(bs, bi, kk, &filled, score_row(qv, C, c_enc, scale, c, d, qv + d), c);
         for (int64_t j = filled; j < kk; ++j) { bs[j] = -INFINITY; bi[j] = -1; }
         free(qv);
     }
@@ -219,10 +227,14 @@ int or_score_pairs(const void *Q, int q_enc, const void *C, int c_enc,
     int err = 0;
 #pragma omp parallel for num_threads(threads) schedule(static)
     for (int64_t p = 0; p < n_pairs; ++p) {
-        double *qv = (double *)malloc(sizeof(double) * (size_t)d);
-        if (!qv) { err = -1; continue; }
+        double *qv = (double *)malloc(sizeof(double) * 2 * (size_t)d);
+        if (!qv) {
+#pragma omp atomic write
+            err = -1;
+            continue;
+        }
         widen_row(Q, q_enc, q_idx[p], d, qv);
-        out[p] = score_row(qv, C, c_enc, scale, c_idx[p], d);
+        out[p] = score_row(qv, C, c_enc, scale, c_idx[p], d, qv + d);
         free(qv);
     }
     return err;
