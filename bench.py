@@ -8,8 +8,9 @@ delivery of every result to each request.  Inputs are synthetic (seeded) and
 resident in HBM before timing starts; the distinct count stays on the device
 (no host synchronisation inside a step).
 
-Default workload: 64 workflows x 32 retrieval queries, query ids Zipf(1.1)
-over 512 templates, d=768 bf16 unit-norm, 1,000,000-chunk bf16 corpus, k=10.
+Default workload (the largest single-GPU one, compute-bound): 512 workflows
+x 64 retrieval queries, query ids Zipf(0.8) over 16,384 templates (about
+10,000 distinct), d=1024 bf16 unit-norm, 4,000,000-chunk bf16 corpus, k=32.
 
 Prints ONE JSON line.  `value` = logical requests per second of the timed
 steps.  `roofline` describes the dominant kernel (the scoring kernel), timed
@@ -33,7 +34,14 @@ METRIC = "merged retrieval queries/s + achieved HBM GB/s or MFMA % (dedup+score+
 PEAK_HBM_GBS = 8000.0
 PEAK_MFMA = {"bf16": 2500.0}          # dense TFLOP/s (no sparsity)
 PEAK_FP32_VECTOR = 157.3              # TFLOP/s, fp32 on the vector units
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_step_ridge1m_traffic.json")
+DEFAULT_WORKLOAD = "mfma4m"
+
+
+def traffic_file(workload: str) -> str:
+    """Committed HBM counter summary of the score step on one workload."""
+    return os.path.join(ROOT, "profiles", f"score_step_{workload}_traffic.json")
+
+
 KERNEL_SOURCES = ["paper_2607_22578_amd/csrc/score_mfma.hip", "paper_2607_22578_amd/csrc/score.hip",
                   "paper_2607_22578_amd/csrc/common.h"]
 # The score step (hs_score_partial) is three launches on one stream: the seed
@@ -71,11 +79,23 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="ridge1m",
-                    help="ridge1m (default), mfma4m, fp8_20m, tiny or dedup256k")
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD,
+                    help="mfma4m (default), ridge1m, fp8_20m, tiny or dedup256k")
+    ap.add_argument("--seed", type=int, default=None,
+                    help="base seed of the synthetic workload (default: 20260722 + the "
+                         "workload's position in the list tiny, ridge1m, dedup256k, mfma4m, "
+                         "fp8_20m)")
+    ap.add_argument("--raw-ids", action="store_true",
+                    help="key-range ablation: request keys are the small template ids "
+                         "themselves instead of 64-bit signature-like values (the dedup may "
+                         "then take its direct-addressing path; the line reports the path)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", type=int, default=96,
-                    help="distinct queries scored by the oracle for the CPU baseline")
+    ap.add_argument("--cpu-sample", type=int, default=0,
+                    help="distinct queries scored by the oracle for the CPU baseline (default: "
+                         "as many as take about 20 s on the oracle's threads)")
+    ap.add_argument("--oracle-threads", type=int, default=0,
+                    help="threads of the CPU baseline (default: OMP_NUM_THREADS if set, else "
+                         "the CPUs this process may run on)")
     ap.add_argument("--no-merge", action="store_true",
                     help="ablation: every request is scored on its own (no dedup merge)")
     ap.add_argument("--corpus-rows", type=int, default=0,
@@ -148,8 +168,13 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     t_gen = time.time()
-    w = synth.make(args.workload, n_corpus=args.corpus_rows or None)
+    w = synth.make(args.workload, seed=args.seed, n_corpus=args.corpus_rows or None)
     t_gen = time.time() - t_gen
+    if args.raw_ids:
+        if args.no_merge:
+            raise SystemExit("--raw-ids and --no-merge exclude each other")
+        # the template id itself as the key: same groups, small key range
+        w.keys = w.template_ids.astype(np.int64).copy()
     if args.no_merge:
         # every request its own key: the same rows and corpus, scored unmerged
         w.keys = np.arange(w.R, dtype=np.int64)
@@ -339,8 +364,10 @@ def main():
     roof["kernel_source"] = src_hash
     if windows is not None:
         roof["note"] = "reuse mode: score-step work priced at the mean miss count"
-    if args.workload == "ridge1m" and os.path.exists(TRAFFIC_FILE):
-        tr = json.load(open(TRAFFIC_FILE))
+    tf = traffic_file(args.workload)
+    if not (args.no_merge or args.raw_ids or args.corpus_rows or windows is not None
+            or args.seed is not None) and os.path.exists(tf):
+        tr = json.load(open(tf))
         if tr.get("kernel_source") == src_hash:
             roof["traffic"] = tr.get("hbm_bytes_per_launch")
 
@@ -354,7 +381,8 @@ def main():
                    "dim": d, "n_corpus": N, "k": k, "query_dtype": cfg.q_enc,
                    "corpus_dtype": cfg.c_enc, "seed": w.seed,
                    "merge": not args.no_merge, "reuse": reuse,
-                   "signatures": args.signatures, "priorities": args.priorities},
+                   "signatures": args.signatures, "priorities": args.priorities,
+                   "raw_ids": args.raw_ids, "dedup_path": dedup_path(w.keys)},
         "unique_queries_per_s": round(n_distinct * args.steps / (total_ms * 1e-3), 1),
         "stages_ms": stages,
         "wall_s_timed": round(wall, 4),
@@ -366,7 +394,7 @@ def main():
         out["priority_step"] = prio_stats
 
     if not args.no_cpu_baseline and windows is None:
-        out["cpu_baseline"] = cpu_baseline(w, n_u, args.cpu_sample)
+        out["cpu_baseline"] = cpu_baseline(w, n_u, args.cpu_sample, args.oracle_threads)
     print(json.dumps(out), flush=True)
 
 
@@ -475,7 +503,7 @@ def dedup_bench(args):
     import synth
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    w = synth.make(args.workload)
+    w = synth.make(args.workload, seed=args.seed)
     R, d = w.R, w.dim
     rows = w.table.shape[0]
     plan = hs.hs_merge_plan(R, d, rows, 1, hs.HS_BF16, hs.HS_BF16)
@@ -554,7 +582,7 @@ def batch_curve_bench(args):
     import synth
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    w = synth.make(args.workload)
+    w = synth.make(args.workload, seed=args.seed)
     cfg = w.cfg
     R, d, N, k = w.R, w.dim, w.n_corpus, w.k
     cdt = {"bf16": hs.HS_BF16, "fp8": hs.HS_FP8_E4M3}[cfg.c_enc]
@@ -664,7 +692,7 @@ def priority_bench(args):
     import synth
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    w = synth.make(args.prio_only, with_corpus=False)
+    w = synth.make(args.prio_only, seed=args.seed, with_corpus=False)
     phi, s_hat, heavy = synth.scheduler_inputs(w)
     R = w.R
     plan = hs.hs_merge_plan(R, 8, 1, 1, hs.HS_BF16, hs.HS_BF16)
@@ -708,37 +736,101 @@ def priority_bench(args):
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(w, n_u: int, n_sample: int) -> dict:
+def oracle_threads(requested: int = 0) -> int:
+    """Threads of the CPU baseline: the request, else OMP_NUM_THREADS, else the
+    CPUs this process may run on."""
+    if requested > 0:
+        return requested
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        return int(env)
+    try:
+        return len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        return os.cpu_count() or 1
+
+
+def host_cpu() -> dict:
+    """The host CPU as lscpu reports it (model name, sockets, cores, threads)."""
+    info = {"model": "", "logical_cpus": os.cpu_count()}
+    try:
+        import subprocess
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            key, _, val = line.partition(":")
+            key, val = key.strip(), val.strip()
+            if key == "Model name":
+                info["model"] = val
+            elif key == "Socket(s)":
+                info["sockets"] = int(val) if val.isdigit() else val
+            elif key == "Core(s) per socket":
+                info["cores_per_socket"] = int(val) if val.isdigit() else val
+            elif key == "Thread(s) per core":
+                info["threads_per_core"] = int(val) if val.isdigit() else val
+    except (OSError, ValueError):
+        pass
+    try:
+        info["affinity_cpus"] = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        pass
+    return info
+
+
+# oracle cost per multiply-add and thread (one sequential fp64 sum per score),
+# used only to size the bounded CPU-baseline sample to about 20 s
+ORACLE_NS_PER_MAC = 1.5
+CPU_BASELINE_TARGET_S = 20.0
+
+
+def cpu_baseline(w, n_u: int, n_sample: int, threads_req: int = 0) -> dict:
     """The oracle on the host: full dedup and representative gather, exact
     scoring + top-k for a seeded sample of distinct queries over the whole
     corpus, extrapolated to all n_u distinct queries."""
     import numpy as np
 
     import oracle
-    threads = oracle.default_threads()
+    threads = oracle_threads(threads_req)
     t0 = time.perf_counter()
     ref = oracle.dedup(w.keys)
     rows = oracle.gather_rows(w.q_req, ref["first_index"])
     t_dedup = time.perf_counter() - t0
     rng = np.random.default_rng(1)
+    if n_sample <= 0:
+        per_query = w.n_corpus * w.dim * ORACLE_NS_PER_MAC * 1e-9
+        n_sample = int(CPU_BASELINE_TARGET_S * threads / max(per_query, 1e-9))
+        n_sample = max(threads, n_sample)
     n_sample = min(n_sample, ref["n_unique"])
     sel = np.sort(rng.choice(ref["n_unique"], size=n_sample, replace=False))
     t1 = time.perf_counter()
     oracle.topk_exact(rows, w.corpus, w.k, scale=w.scale, q_rows=sel, threads=threads)
     t_score = time.perf_counter() - t1
     t_full = t_dedup + t_score * ref["n_unique"] / n_sample
-    cpu = ""
-    try:
-        with open("/proc/cpuinfo") as f:
-            cpu = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
-    except OSError:
-        pass
+    cpu = host_cpu()
     return {"value": round(w.R / t_full, 2), "unit": "queries/s", "cores": threads,
-            "kind": "oracle", "cpu_model": cpu,
+            "kind": "oracle", "cpu_model": cpu.get("model", ""), "host": cpu,
             "sample": f"dedup+gather of all {w.R} requests, exact fp64 top-{w.k} of "
                       f"{n_sample}/{ref['n_unique']} distinct queries over all {w.n_corpus} "
-                      f"rows ({t_score:.1f} s), extrapolated to all distinct queries",
+                      f"rows ({t_score:.1f} s on {threads} threads), extrapolated to all "
+                      "distinct queries",
             "measured_s": round(t_dedup + t_score, 2)}
+
+
+# The dedup path hs_dedup takes for a window's keys (the rule documented with
+# hs_dedup): one workgroup up to 4,096 requests (hash table up to 2,048), then
+# direct addressing when max - min < R, else an LSD radix sort with one pass
+# per 8 bits of max - min.
+def dedup_path(keys) -> str:
+    import numpy as np
+    R = int(keys.shape[0])
+    if R <= 2048:
+        return "lds-hash (one workgroup)"
+    if R <= 4096:
+        return "bitonic (one workgroup)"
+    span = int(np.max(keys)) - int(np.min(keys))
+    if span < R:
+        return f"direct addressing (key range {span + 1})"
+    passes = max(1, (span.bit_length() + 7) // 8)
+    return f"radix ({passes} passes of 8 bits)"
 
 
 if __name__ == "__main__":

@@ -11,16 +11,18 @@
  *     every related query (Topological Fusion within Time Window);
  *   - same-type ready nodes execute as one batch (Appendix A, batching
  *     constraint: b <= B_r, only nodes with consistent profile).
- * The library runs that window as four device steps on a caller stream:
+ * The library runs that window as device steps on a caller stream:
  *   hs_dedup       group the R request keys (signatures) -> distinct keys,
  *                  survivor per group, group sizes |M(v*)| (Eq. 3), and the
  *                  redirect map request -> group;
- *   hs_scatter     row gather: representative query rows, embedding rows of
- *                  distinct chunk ids, and delivery of results to requests;
+ *   hs_scatter     row gather: representative query rows and embedding rows
+ *                  of distinct chunk ids;
  *   hs_score_topk  exact inner-product top-k of every distinct query against
  *                  the corpus (retrieval with Top-K among its parameters,
  *                  Eq. 2; top-K vector retrieval of the RAG workloads, Sec. 4.1)
- *                  = hs_score_partial followed by hs_topk_merge.
+ *                  = hs_score_partial followed by hs_topk_merge;
+ *   hs_deliver     every request receives its group's result, each
+ *                  workflow's requests in one contiguous row range.
  * Optionally, hs_cache_lookup / hs_cache_insert reuse results across windows
  * (Sec. 3.3 (II)), so that only keys not seen before are scored,
  * hs_signature computes the keys themselves from node descriptions (Eq. 2),
@@ -54,7 +56,7 @@
 extern "C" {
 #endif
 
-#define HS_ABI_VERSION 1
+#define HS_ABI_VERSION 2
 
 typedef enum {
     HS_OK = 0,
@@ -83,8 +85,21 @@ typedef struct {
     int32_t corpus_dtype; /* HS_F32 (with F32 queries), HS_BF16 or HS_FP8_E4M3
                              (with BF16 queries) */
     int32_t flags;        /* reserved, must be 0 */
-    int64_t max_unique;   /* upper bound on distinct keys (0 = n_requests); the
-                             batch limit B_r of Appendix A when the caller sets it */
+    int64_t max_unique;   /* batch limit B_r of Appendix A (0 = n_requests): the
+                             score step handles at most this many distinct
+                             queries per call; a window with more distinct keys
+                             is scored in several batches (see hs_score_topk) */
+    int64_t n_workflows;  /* W >= 1: workflows that issued the window's requests
+                             (Sec. 3.3 (I): the fused nodes of several
+                             concurrent workflows) */
+    const int64_t *workflow_offsets;
+                          /* host CSR [W + 1], may be NULL: workflow w issued
+                             requests [off[w], off[w+1]) (arrival order is
+                             workflow-major), so its results are those rows of
+                             the per-request outputs.  off[0] = 0, non-decreasing,
+                             off[W] = n_requests.  NULL = uniform: W divides
+                             n_requests and every workflow has n_requests / W.
+                             Read and copied during hs_merge_plan only. */
 } hs_merge_desc;
 
 typedef struct hs_plan hs_plan;   /* opaque, immutable, thread-safe host object */
@@ -92,10 +107,17 @@ typedef struct hs_plan hs_plan;   /* opaque, immutable, thread-safe host object 
 /* Validate `desc` and create a plan.  *workspace_bytes receives the size of the
  * device workspace that hs_dedup and hs_score_topk (and its two phases) need
  * for this shape (it also covers hs_priority).  The plan is freed with
- * hs_plan_destroy. */
+ * hs_plan_destroy.  Bad workflow offsets (wrong first or last entry, a
+ * decreasing entry, W not dividing R when they are NULL) are rejected with
+ * HS_ERR_INVALID_ARG. */
 hs_status hs_merge_plan(const hs_merge_desc *desc, hs_plan **plan, size_t *workspace_bytes);
 
 void hs_plan_destroy(hs_plan *plan);
+
+/* Rows of workflow w (0 <= w < W) in the per-request outputs (hs_deliver):
+ * [*first, *first + *count).  Host only, no device work (Sec. 3.3 (I): each
+ * workflow's merged nodes receive the survivors' outputs). */
+hs_status hs_workflow_rows(const hs_plan *plan, int64_t w, int64_t *first, int64_t *count);
 
 /* Step 1 -- signature matching (Sec. 3.3 (I); Appendix B.3, Phase 1: duplicate
  * detection through a global duplication map).
@@ -109,7 +131,13 @@ void hs_plan_destroy(hs_plan *plan);
  *   n_unique_host int64 host out, may be NULL: if given, the call waits for
  *                 the stream once and stores n_u there
  * Entries [n_u, R) of the per-group outputs are left unspecified.  R = 0 sets
- * n_u = 0.  Bit-exact and deterministic. */
+ * n_u = 0.  Bit-exact and deterministic.  n_unique_dev (and n_unique_host)
+ * always hold the full count, even when it exceeds max_unique.
+ * Method (for any int64 keys; the outputs do not depend on it): one workgroup
+ * for R <= 4,096 (an LDS hash table up to 2,048 requests, else a bitonic sort);
+ * above, the key range is found on the device and the keys are numbered by
+ * direct addressing when max - min < R, else sorted by an LSD radix sort with
+ * one pass per 8 bits of max - min. */
 hs_status hs_dedup(const hs_plan *plan, const int64_t *keys, int64_t *unique_keys,
                    int32_t *first_index, int32_t *counts, int32_t *inverse,
                    int64_t *n_unique_dev, int64_t *n_unique_host,
@@ -127,7 +155,13 @@ hs_status hs_dedup(const hs_plan *plan, const int64_t *keys, int64_t *unique_key
  *   topk_index    [n_u x k] int32 device out: corpus rows; equal scores are
  *                 ordered by ascending row; slots beyond N are (-inf, -1)
  * Scores accumulate in fp32 from exact bf16/fp8 products (fp32 products for
- * F32 inputs).  Identical corpus rows get bit-identical scores. */
+ * F32 inputs).  Identical corpus rows get bit-identical scores.
+ * One call is one batch of at most max_unique distinct queries (B_r): with
+ * n_unique = -1 it scores the first min(n_u, max_unique) rows of q_unique.  A
+ * window with more distinct keys than max_unique (n_unique_dev tells) is
+ * scored in further calls on the following rows, with host counts and
+ * pointers advanced by the batch (topk_score/index then need room for n_u
+ * rows). */
 hs_status hs_score_topk(const hs_plan *plan, const void *q_unique, int64_t n_unique,
                         const int64_t *n_unique_dev, const void *corpus,
                         const float *row_scale, float *topk_score, int32_t *topk_index,
@@ -150,12 +184,14 @@ hs_status hs_topk_merge(const hs_plan *plan, int64_t n_unique, const int64_t *n_
                         float *topk_score, int32_t *topk_index,
                         void *ws, size_t ws_bytes, void *stream);
 
-/* Steps 2, 2' and 5 -- row gather dst[i] = src[index[i]], i < n_rows.
- * The race-free form of delivering one result to many nodes (Sec. 3.3 (I):
- * the survivor's output flows to all related queries):
+/* Steps 2 and 2' -- row gather dst[i] = src[index[i]], i < n_rows.
+ * The race-free form of handing one row to many consumers (Sec. 3.3 (I): one
+ * execution instance per merged set, its output flowing to all related
+ * queries):
  *   representative rows: src = request queries,  index = first_index
  *   embedding rows:      src = embedding table,  index = unique_keys (int64)
- *   delivery:            src = topk_score/index, index = inverse
+ *   one delivered array: src = topk_score or topk_index, index = inverse
+ *                        (hs_deliver does both arrays in one launch)
  *   src        [src_rows x row_bytes] device
  *   row_bytes  > 0 and a multiple of 4 (16-byte rows use 128-bit accesses)
  *   index      [n_out] int32 (index_is_i64 = 0) or int64 (= 1) device
@@ -167,6 +203,21 @@ hs_status hs_topk_merge(const hs_plan *plan, int64_t n_unique, const int64_t *n_
 hs_status hs_scatter(const void *src, int64_t src_rows, int64_t row_bytes,
                      const void *index, int32_t index_is_i64, int64_t n_out,
                      const int64_t *n_out_dev, void *dst, void *stream);
+
+/* Step 5 -- delivery (Sec. 3.3 (I): the survivor's output flows to the
+ * downstream nodes of every merged query): for every request i < R,
+ *   out_score[i] = topk_score[inverse[i]], out_index[i] = topk_index[inverse[i]]
+ * (k entries each, the plan's R and k), in one launch.
+ *   topk_score/index [topk_rows x k] device: results of the distinct queries
+ *   topk_rows       rows held by topk_score/index (>= 0); a request whose group
+ *                   is outside [0, topk_rows) is left unwritten
+ *   inverse         [R] int32 device: hs_dedup's request -> group map
+ *   out_score/index [R x k] device out: per-request results; workflow w's
+ *                   requests are rows hs_workflow_rows(plan, w)
+ * Bit-exact copies. */
+hs_status hs_deliver(const hs_plan *plan, const float *topk_score, const int32_t *topk_index,
+                     int64_t topk_rows, const int32_t *inverse, float *out_score,
+                     int32_t *out_index, void *stream);
 
 /* Cross-window reuse (Sec. 3.3 (II), asynchronous cache reuse): a node whose
  * signature matches a node completed in an earlier window takes that node's

@@ -33,10 +33,10 @@ _lib = ctypes.CDLL(LIB_PATH)
 HS_OK, HS_ERR_INVALID_ARG, HS_ERR_UNSUPPORTED, HS_ERR_WORKSPACE, HS_ERR_ALIGNMENT, \
     HS_ERR_DEVICE = range(6)
 HS_F32, HS_BF16, HS_FP8_E4M3 = 0, 1, 2
-ABI_VERSION = 1
+ABI_VERSION = 2
 
-EXPORTS = ["hs_merge_plan", "hs_plan_destroy", "hs_dedup", "hs_score_topk", "hs_score_partial",
-           "hs_topk_merge", "hs_scatter", "hs_cache_bytes", "hs_cache_reset", "hs_cache_lookup",
+EXPORTS = ["hs_merge_plan", "hs_plan_destroy", "hs_workflow_rows", "hs_dedup", "hs_score_topk",
+           "hs_score_partial", "hs_topk_merge", "hs_scatter", "hs_deliver", "hs_cache_bytes", "hs_cache_reset", "hs_cache_lookup",
            "hs_cache_insert", "hs_signature", "hs_priority", "hs_status_string",
            "hs_last_error", "hs_abi_version"]
 HS_SIG_NORMALIZE_TEXT = 1
@@ -46,7 +46,9 @@ class hs_merge_desc(ctypes.Structure):
     _fields_ = [("n_requests", ctypes.c_int64), ("dim", ctypes.c_int64),
                 ("n_corpus", ctypes.c_int64), ("k", ctypes.c_int32),
                 ("query_dtype", ctypes.c_int32), ("corpus_dtype", ctypes.c_int32),
-                ("flags", ctypes.c_int32), ("max_unique", ctypes.c_int64)]
+                ("flags", ctypes.c_int32), ("max_unique", ctypes.c_int64),
+                ("n_workflows", ctypes.c_int64),
+                ("workflow_offsets", ctypes.POINTER(ctypes.c_int64))]
 
 
 class hs_sig_nodes(ctypes.Structure):
@@ -64,6 +66,10 @@ _lib.hs_merge_plan.argtypes = [ctypes.POINTER(hs_merge_desc), ctypes.POINTER(_vp
 _lib.hs_merge_plan.restype = ctypes.c_int
 _lib.hs_plan_destroy.argtypes = [_vp]
 _lib.hs_plan_destroy.restype = None
+_lib.hs_workflow_rows.argtypes = [_vp, _i64, ctypes.POINTER(_i64), ctypes.POINTER(_i64)]
+_lib.hs_workflow_rows.restype = ctypes.c_int
+_lib.hs_deliver.argtypes = [_vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp]
+_lib.hs_deliver.restype = ctypes.c_int
 _lib.hs_dedup.argtypes = [_vp] + [_vp] * 7 + [_vp, _sz, _vp]
 _lib.hs_dedup.restype = ctypes.c_int
 _lib.hs_score_topk.argtypes = [_vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
@@ -159,12 +165,35 @@ class Plan:
 
 
 def hs_merge_plan(n_requests: int, dim: int, n_corpus: int, k: int, query_dtype: int,
-                  corpus_dtype: int, max_unique: int = 0, flags: int = 0) -> Plan:
-    d = hs_merge_desc(n_requests, dim, n_corpus, k, query_dtype, corpus_dtype, flags, max_unique)
+                  corpus_dtype: int, max_unique: int = 0, flags: int = 0,
+                  n_workflows: int = 1, workflow_offsets=None) -> Plan:
+    """workflow_offsets: None (uniform) or a sequence of n_workflows + 1
+    request offsets (host CSR)."""
+    off = None
+    if workflow_offsets is not None:
+        vals = [int(x) for x in workflow_offsets]
+        off = (ctypes.c_int64 * max(len(vals), 1))(*vals)
+    d = hs_merge_desc(n_requests, dim, n_corpus, k, query_dtype, corpus_dtype, flags, max_unique,
+                      n_workflows, ctypes.cast(off, ctypes.POINTER(ctypes.c_int64))
+                      if off is not None else None)
     h = _vp()
     ws = _sz()
     _check(_lib.hs_merge_plan(ctypes.byref(d), ctypes.byref(h), ctypes.byref(ws)))
+    d.workflow_offsets = None   # the plan keeps its own copy
     return Plan(h.value, int(ws.value), d)
+
+
+def hs_workflow_rows(plan: Plan, w: int):
+    """(first, count): rows of workflow w in the per-request outputs."""
+    a, b = _i64(), _i64()
+    _check(_lib.hs_workflow_rows(plan.handle, w, ctypes.byref(a), ctypes.byref(b)))
+    return int(a.value), int(b.value)
+
+
+def hs_deliver(plan: Plan, topk_score, topk_index, topk_rows: int, inverse, out_score, out_index,
+               stream=None):
+    _check(_lib.hs_deliver(plan.handle, _ptr(topk_score), _ptr(topk_index), topk_rows,
+                           _ptr(inverse), _ptr(out_score), _ptr(out_index), _stream(stream)))
 
 
 def hs_dedup(plan: Plan, keys, unique_keys, first_index, counts, inverse, n_unique_dev,
@@ -285,12 +314,15 @@ class MergedRetrieval:
     on one stream.  All outputs are torch tensors on the device."""
 
     def __init__(self, n_requests: int, dim: int, n_corpus: int, k: int, query_dtype: int,
-                 corpus_dtype: int, device="cuda", max_unique: int = 0):
+                 corpus_dtype: int, device="cuda", max_unique: int = 0, n_workflows: int = 1,
+                 workflow_offsets=None):
         import torch
         self.R, self.d, self.N, self.k = n_requests, dim, n_corpus, k
         self.qdt, self.cdt = query_dtype, corpus_dtype
         self.plan = hs_merge_plan(n_requests, dim, n_corpus, k, query_dtype, corpus_dtype,
-                                  max_unique)
+                                  max_unique, n_workflows=n_workflows,
+                                  workflow_offsets=workflow_offsets)
+        self.n_workflows = n_workflows
         cap = max_unique if max_unique > 0 else n_requests
         self.cap = cap
         dev = torch.device(device)
@@ -302,9 +334,11 @@ class MergedRetrieval:
         self.counts = torch.empty(R1, dtype=torch.int32, device=dev)
         self.inverse = torch.empty(R1, dtype=torch.int32, device=dev)
         self.n_unique = torch.zeros(1, dtype=torch.int64, device=dev)
-        self.q_unique = torch.empty((max(cap, 1), dim), dtype=qt, device=dev)
-        self.topk_score = torch.empty((max(cap, 1), k), dtype=torch.float32, device=dev)
-        self.topk_index = torch.empty((max(cap, 1), k), dtype=torch.int32, device=dev)
+        # rows for every distinct query of a window (more than one batch of
+        # max_unique when the window has more distinct keys)
+        self.q_unique = torch.empty((R1, dim), dtype=qt, device=dev)
+        self.topk_score = torch.empty((R1, k), dtype=torch.float32, device=dev)
+        self.topk_index = torch.empty((R1, k), dtype=torch.int32, device=dev)
         self.out_score = torch.empty((R1, k), dtype=torch.float32, device=dev)
         self.out_index = torch.empty((R1, k), dtype=torch.int32, device=dev)
         self.q_row_bytes = dim * (4 if query_dtype == HS_F32 else 2)
@@ -327,14 +361,28 @@ class MergedRetrieval:
                       self.ws, stream=stream)
 
     def deliver(self, stream=None):
-        hs_scatter(self.topk_score, self.cap, self.k * 4, self.inverse, 0, self.R, None,
-                   self.out_score, stream=stream)
-        hs_scatter(self.topk_index, self.cap, self.k * 4, self.inverse, 0, self.R, None,
-                   self.out_index, stream=stream)
+        hs_deliver(self.plan, self.topk_score, self.topk_index, self.topk_score.shape[0],
+                   self.inverse, self.out_score, self.out_index, stream=stream)
+
+    def workflow_results(self, w: int):
+        """(scores, indices) of workflow w's requests: views of its rows of
+        the per-request outputs."""
+        first, count = hs_workflow_rows(self.plan, w)
+        return (self.out_score[first:first + count], self.out_index[first:first + count])
 
     def run(self, keys, q_req, corpus, scale=None, stream=None, n_unique: int = -1):
         """The whole window; n_unique = -1 keeps the distinct count on the
-        device (no host synchronisation)."""
+        device (no host synchronisation).  With max_unique below the number
+        of requests, the distinct count is read on the host (one
+        synchronisation) and the distinct queries are scored in batches of at
+        most max_unique (B_r), so that no group is left unscored."""
+        if self.cap < self.R:
+            nu = self.dedup(keys, stream, host_count=True)
+            hs_scatter(q_req, self.R, self.q_row_bytes, self.first_index, 0, self.R,
+                       self.n_unique, self.q_unique, stream=stream)
+            self.score_chunked(corpus, nu, self.cap, scale, stream)
+            self.deliver(stream)
+            return
         self.dedup(keys, stream)
         self.gather_queries(q_req, stream)
         self.score_partial(corpus, scale, n_unique, stream)
@@ -366,6 +414,9 @@ class MergedRetrieval:
         score/top-k of the misses -> miss rows put in place -> store insert ->
         delivery.  Distinct and miss counts stay on the device.  score_events
         = (start, end) events recorded around the score step, if given."""
+        if self.cap < self.R:
+            raise ValueError("run_cached scores one batch per window: it needs max_unique = 0 "
+                             "(or n_requests)")
         self.dedup(keys, stream)
         hs_cache_lookup(self.plan, self.cache, self.cache_capacity, self.unique_keys,
                         self.first_index, -1, self.n_unique, self.topk_score, self.topk_index,

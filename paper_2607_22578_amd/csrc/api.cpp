@@ -11,6 +11,7 @@
 #include <cstdio>
 #include <cstring>
 #include <new>
+#include <vector>
 
 #include "../../include/hs_merge.h"
 
@@ -21,6 +22,8 @@ hipError_t launch_dedup(const int64_t *keys, int64_t R, int64_t *uk, int32_t *fi
 hipError_t launch_gather(const void *src, int64_t src_rows, int64_t row_bytes, const void *index,
                          int is64, int64_t n_out, const int64_t *n_out_dev, void *dst,
                          hipStream_t st);
+hipError_t launch_deliver(const float *ts, const int32_t *ti, int64_t rows, const int32_t *inv,
+                          int64_t R, int k, float *os, int32_t *oi, hipStream_t st);
 size_t score_workspace_bytes(int64_t cap, int64_t N, int k, int corpus_dtype);
 hipError_t launch_score_partial(const void *q, const void *corpus, const float *scale, int64_t N,
                                 int64_t d, int k, int64_t n_unique, const int64_t *nu_dev,
@@ -53,7 +56,8 @@ hipError_t launch_priority(const int32_t *inverse, const int32_t *first_index, i
 }  // namespace hs
 
 struct hs_plan {
-  hs_merge_desc d;
+  hs_merge_desc d;      // (d.workflow_offsets is not kept: see offsets)
+  std::vector<int64_t> offsets;   // workflow CSR [W + 1]
   int64_t cap;          // max distinct keys
   size_t ws_dedup;      // bytes used by hs_dedup (offset 0)
   size_t ws_score;      // bytes used by the score phases (offset 0)
@@ -135,9 +139,37 @@ hs_status hs_merge_plan(const hs_merge_desc *desc, hs_plan **plan, size_t *works
     return fail(HS_ERR_UNSUPPORTED, "hs_merge_plan: BF16 needs dim %% 8 == 0");
   if (d.corpus_dtype == HS_FP8_E4M3 && d.dim % 16 != 0)
     return fail(HS_ERR_UNSUPPORTED, "hs_merge_plan: FP8 corpus needs dim %% 16 == 0");
+  if (d.n_workflows < 1 || d.n_workflows > ((int64_t)1 << 30))
+    return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: n_workflows %lld out of [1, 2^30]",
+                (long long)d.n_workflows);
+  const int64_t W = d.n_workflows;
+  if (d.workflow_offsets) {
+    const int64_t *o = d.workflow_offsets;
+    if (o[0] != 0 || o[W] != d.n_requests)
+      return fail(HS_ERR_INVALID_ARG,
+                  "hs_merge_plan: workflow_offsets must start at 0 and end at n_requests "
+                  "(got %lld and %lld)", (long long)o[0], (long long)o[W]);
+    for (int64_t w = 0; w < W; ++w)
+      if (o[w + 1] < o[w])
+        return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: workflow_offsets decrease at %lld",
+                    (long long)w);
+  } else if (d.n_requests % W != 0) {
+    return fail(HS_ERR_INVALID_ARG,
+                "hs_merge_plan: %lld workflows do not divide %lld requests (pass "
+                "workflow_offsets)", (long long)W, (long long)d.n_requests);
+  }
   hs_plan *p = new (std::nothrow) hs_plan;
   if (!p) return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: out of host memory");
+  try {
+    p->offsets.resize((size_t)W + 1);
+  } catch (...) {
+    delete p;
+    return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: out of host memory");
+  }
+  for (int64_t w = 0; w <= W; ++w)
+    p->offsets[(size_t)w] = d.workflow_offsets ? d.workflow_offsets[w] : w * (d.n_requests / W);
   p->d = d;
+  p->d.workflow_offsets = nullptr;
   p->cap = d.max_unique > 0 ? d.max_unique : d.n_requests;
   p->ws_dedup = hs::dedup_workspace_bytes(d.n_requests);
   p->ws_score = hs::score_workspace_bytes(p->cap, d.n_corpus, d.k, d.corpus_dtype);
@@ -150,6 +182,16 @@ hs_status hs_merge_plan(const hs_merge_desc *desc, hs_plan **plan, size_t *works
 }
 
 void hs_plan_destroy(hs_plan *plan) { delete plan; }
+
+hs_status hs_workflow_rows(const hs_plan *plan, int64_t w, int64_t *first, int64_t *count) {
+  if (!plan || !first || !count) return fail(HS_ERR_INVALID_ARG, "hs_workflow_rows: null argument");
+  if (w < 0 || w >= plan->d.n_workflows)
+    return fail(HS_ERR_INVALID_ARG, "hs_workflow_rows: workflow %lld out of [0, %lld)",
+                (long long)w, (long long)plan->d.n_workflows);
+  *first = plan->offsets[(size_t)w];
+  *count = plan->offsets[(size_t)w + 1] - plan->offsets[(size_t)w];
+  return ok();
+}
 
 hs_status hs_dedup(const hs_plan *plan, const int64_t *keys, int64_t *unique_keys,
                    int32_t *first_index, int32_t *counts, int32_t *inverse,
@@ -291,6 +333,23 @@ hs_status hs_scatter(const void *src, int64_t src_rows, int64_t row_bytes, const
   hipError_t e = hs::launch_gather(src, src_rows, row_bytes, index, index_is_i64, n_out,
                                    n_out_dev, dst, (hipStream_t)stream);
   return device_status(e, "hs_scatter launch");
+}
+
+hs_status hs_deliver(const hs_plan *plan, const float *topk_score, const int32_t *topk_index,
+                     int64_t topk_rows, const int32_t *inverse, float *out_score,
+                     int32_t *out_index, void *stream) {
+  if (!plan) return fail(HS_ERR_INVALID_ARG, "hs_deliver: null plan");
+  if (topk_rows < 0) return fail(HS_ERR_INVALID_ARG, "hs_deliver: negative topk_rows");
+  const int64_t R = plan->d.n_requests;
+  if (R == 0 || topk_rows == 0) return ok();
+  if (!topk_score || !topk_index || !inverse || !out_score || !out_index)
+    return fail(HS_ERR_INVALID_ARG, "hs_deliver: null argument");
+  if (!aligned(topk_score, 4) || !aligned(topk_index, 4) || !aligned(inverse, 4) ||
+      !aligned(out_score, 4) || !aligned(out_index, 4))
+    return fail(HS_ERR_ALIGNMENT, "hs_deliver: misaligned pointer");
+  hipError_t e = hs::launch_deliver(topk_score, topk_index, topk_rows, inverse, R, plan->d.k,
+                                    out_score, out_index, (hipStream_t)stream);
+  return device_status(e, "hs_deliver launch");
 }
 
 // ---------------------------------------------------------------- result store

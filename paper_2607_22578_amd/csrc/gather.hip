@@ -1,4 +1,4 @@
-// Steps 2, 2' and 5: row gather dst[i] = src[index[i]].
+// Steps 2 and 2': row gather dst[i] = src[index[i]]; step 5: delivery.
 //
 // HeraSys Sec. 3.3 (I): the surviving node runs once and its output flows to
 // the downstream nodes of every related query.  Expressed as a gather (each
@@ -66,6 +66,38 @@ hipError_t launch_gather(const void *src, int64_t src_rows, int64_t row_bytes, c
                                   st);
   return launch_gather_t<uint32_t>(src, src_rows, row_bytes, index, is64, n_out, n_out_dev, dst,
                                    st);
+}
+
+// Step 5 in one launch: request i receives the k results of its group,
+// out[i * k + j] = topk[inverse[i] * k + j] for scores and indices.  One
+// thread per output element, so consecutive threads read and write
+// consecutive elements of a row; groups outside [0, rows) are skipped.
+__global__ __launch_bounds__(256) void deliver_kernel(const float *__restrict__ ts,
+                                                      const int32_t *__restrict__ ti,
+                                                      int64_t rows, const int32_t *__restrict__ inv,
+                                                      int64_t R, int k, float *__restrict__ os,
+                                                      int32_t *__restrict__ oi) {
+  const int64_t total = R * k;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * 256) {
+    const int64_t i = e / k;
+    const int64_t g = inv[i];
+    if (g < 0 || g >= rows) continue;
+    const int64_t src = g * k + (e - i * k);
+    os[e] = ts[src];
+    oi[e] = ti[src];
+  }
+}
+
+hipError_t launch_deliver(const float *ts, const int32_t *ti, int64_t rows, const int32_t *inv,
+                          int64_t R, int k, float *os, int32_t *oi, hipStream_t st) {
+  const int64_t total = R * (int64_t)k;
+  if (total <= 0) return hipSuccess;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 16384) blocks = 16384;
+  hipLaunchKernelGGL(deliver_kernel, dim3((unsigned)blocks), dim3(256), 0, st, ts, ti, rows, inv,
+                     R, k, os, oi);
+  return hipGetLastError();
 }
 
 }  // namespace hs

@@ -26,7 +26,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert hs.hs_abi_version() == hs.ABI_VERSION == 1
+    assert hs.hs_abi_version() == hs.ABI_VERSION == 2
     assert hs.hs_status_string(hs.HS_OK) == "HS_OK"
     assert hs.hs_status_string(hs.HS_ERR_WORKSPACE) == "HS_ERR_WORKSPACE"
     assert hs.hs_status_string(99) == "HS_ERR_UNKNOWN"
@@ -70,7 +70,59 @@ def test_plan_rejects(bad, code):
     assert hs.hs_last_error()
 
 
+def test_workflow_offsets_uniform_and_csr():
+    # NULL offsets: W equal workflows of R / W requests
+    p = hs.hs_merge_plan(**GOOD, n_workflows=64)
+    assert [hs.hs_workflow_rows(p, w) for w in (0, 1, 63)] == [(0, 32), (32, 32), (2016, 32)]
+    # an explicit CSR (empty workflows allowed), copied by the plan
+    off = [0, 5, 5, 1000, 2048]
+    p = hs.hs_merge_plan(**GOOD, n_workflows=4, workflow_offsets=off)
+    off[1] = 999   # the caller's array is not kept
+    assert [hs.hs_workflow_rows(p, w) for w in range(4)] == [(0, 5), (5, 0), (5, 995),
+                                                             (1000, 1048)]
+    for w in (-1, 4):
+        with pytest.raises(hs.HsError) as e:
+            hs.hs_workflow_rows(p, w)
+        assert e.value.status == hs.HS_ERR_INVALID_ARG
+    # one workflow holding the whole (possibly empty) window
+    assert hs.hs_workflow_rows(hs.hs_merge_plan(**dict(GOOD, n_requests=0)), 0) == (0, 0)
+
+
+@pytest.mark.parametrize("W,off", [
+    (0, None),                      # at least one workflow
+    (-3, None),
+    (2 ** 30 + 1, None),
+    (3, None),                      # 3 does not divide 2048 without offsets
+    (3, [1, 5, 9, 2048]),           # must start at 0
+    (3, [0, 5, 9, 2047]),           # must end at R
+    (3, [0, 9, 5, 2048]),           # decreasing
+    (2, [0, 2049, 2048]),           # decreasing at the end
+])
+def test_workflow_offsets_rejected(W, off):
+    with pytest.raises(hs.HsError) as e:
+        hs.hs_merge_plan(**GOOD, n_workflows=W, workflow_offsets=off)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    assert "workflow" in hs.hs_last_error()
+
+
 FAKE = 0x10000000   # never dereferenced: validation fails first
+
+
+def test_deliver_validation():
+    p = hs.hs_merge_plan(**GOOD)
+    hs.hs_deliver(p, FAKE, FAKE, 0, FAKE, FAKE, FAKE)   # no rows: nothing enqueued
+    with pytest.raises(hs.HsError) as e:
+        hs.hs_deliver(p, FAKE, FAKE, -1, FAKE, FAKE, FAKE)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    with pytest.raises(hs.HsError) as e:
+        hs.hs_deliver(p, FAKE, None, 10, FAKE, FAKE, FAKE)
+    assert e.value.status == hs.HS_ERR_INVALID_ARG
+    with pytest.raises(hs.HsError) as e:
+        hs.hs_deliver(p, FAKE, FAKE, 10, FAKE + 2, FAKE, FAKE)
+    assert e.value.status == hs.HS_ERR_ALIGNMENT
+    # a null plan, through the C entry point itself
+    assert hs._lib.hs_deliver(None, FAKE, FAKE, 10, FAKE, FAKE, FAKE, None) == \
+        hs.HS_ERR_INVALID_ARG
 
 
 def test_dedup_validation():

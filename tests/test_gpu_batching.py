@@ -67,3 +67,36 @@ def test_split_on_streams_equals_one_batch(parts):
     s2, i2 = _snapshot(m, nu)
     np.testing.assert_array_equal(i2, i1)
     np.testing.assert_array_equal(s2, s1)
+
+
+def test_max_unique_below_distinct_count_scores_every_group():
+    """A batch limit B_r (max_unique) below the window's distinct count: the
+    composition reads the count and scores the distinct queries in batches
+    of at most B_r, so every request gets its result -- identical to the
+    unlimited plan (and accepted by the oracle for a sample)."""
+    import paper_2607_22578_amd as hs
+    dev = device()
+    w = synth.make("ridge1m", n_corpus=1, with_corpus=False)
+    N = 9_000
+    c, _ = synth.gaussian_rows(w.seed, synth.S_CORPUS, N, w.dim, "bf16")
+    st = torch.cuda.current_stream(dev)
+    kd, qd, cd = to_dev(w.keys), to_dev(w.q_req), to_dev(c)
+    outs = []
+    for cap in (0, 64, 200):
+        m = hs.MergedRetrieval(w.R, w.dim, N, w.k, hs.HS_BF16, hs.HS_BF16, device=dev,
+                               max_unique=cap)
+        m.out_score.fill_(float("nan"))
+        m.out_index.fill_(-7)
+        m.run(kd, qd, cd, stream=st)
+        torch.cuda.synchronize(dev)
+        outs.append((m.out_score.cpu().numpy().view(np.uint32).copy(),
+                     m.out_index.cpu().numpy().copy()))
+        if cap:
+            nu = int(m.n_unique.item())
+            assert nu > cap   # the limit is really below the distinct count
+            ref = check_dedup(m, w.keys)
+            check_unique_topk(m, ref, w.q_req, c, w.k, sel=np.array([0, cap - 1, cap, nu - 1]))
+    assert np.all(outs[0][1] >= 0)
+    for s, i in outs[1:]:
+        np.testing.assert_array_equal(i, outs[0][1])
+        np.testing.assert_array_equal(s, outs[0][0])

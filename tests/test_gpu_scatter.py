@@ -67,3 +67,34 @@ def test_gather_rows_widths(row_bytes, is64):
     want = oracle.gather_rows(src, np.where(ok, idx, 0).astype(idx.dtype))
     np.testing.assert_array_equal(got[ok], want[ok])
     assert np.all(got[~ok] == 0xFFFFFFFF)
+
+
+def test_deliver_both_arrays_and_workflow_rows():
+    """hs_deliver: out[i] = topk[inverse[i]] for scores and indices in one
+    launch, bit-exact against the oracle's gather; groups outside the topk
+    rows leave their requests untouched; workflow w's requests are the rows
+    hs_workflow_rows names."""
+    import paper_2607_22578_amd as hs
+    dev = device()
+    rng = np.random.default_rng(5)
+    R, k, rows = 3001, 13, 400
+    off = np.concatenate([[0], np.sort(rng.integers(0, R, 6)), [R]]).astype(np.int64)
+    plan = hs.hs_merge_plan(R, 8, 1000, k, hs.HS_BF16, hs.HS_BF16, n_workflows=len(off) - 1,
+                            workflow_offsets=off)
+    ts = rng.standard_normal((rows, k)).astype(np.float32)
+    ti = rng.integers(0, 1000, (rows, k)).astype(np.int32)
+    inv = rng.integers(0, rows, R).astype(np.int32)
+    inv[[3, 77]] = rows          # outside: left unwritten
+    inv[100] = -1
+    os_ = torch.full((R, k), 0.5, dtype=torch.float32, device=dev)
+    oi = torch.full((R, k), -9, dtype=torch.int32, device=dev)
+    hs.hs_deliver(plan, to_dev(ts), to_dev(ti), rows, to_dev(inv), os_, oi)
+    torch.cuda.synchronize(dev)
+    ok = (inv >= 0) & (inv < rows)
+    got_s, got_i = os_.cpu().numpy(), oi.cpu().numpy()
+    np.testing.assert_array_equal(got_s[ok].view(np.uint32),
+                                  oracle.gather_rows(ts, inv[ok]).view(np.uint32))
+    np.testing.assert_array_equal(got_i[ok], oracle.gather_rows(ti, inv[ok]))
+    assert np.all(got_s[~ok] == 0.5) and np.all(got_i[~ok] == -9)
+    for wf in range(len(off) - 1):
+        assert hs.hs_workflow_rows(plan, wf) == (int(off[wf]), int(off[wf + 1] - off[wf]))
