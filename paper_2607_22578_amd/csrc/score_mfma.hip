@@ -211,6 +211,11 @@ __device__ __forceinline__ void dma4(i32x4m rsrc, const void *lds, uint32_t voff
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
                :: "s"(l), "v"(voff), "s"(rsrc) : "memory", "m0");
 }
+__device__ __forceinline__ void dma16s(i32x4m rsrc, uint32_t lds, uint32_t voff) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane(lds);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(l), "v"(voff), "s"(rsrc) : "memory", "m0");
+}
 #pragma clang diagnostic pop
 
 struct MfmaArgs {
@@ -237,36 +242,38 @@ struct Frag {
   // bf16: A pieces [step][rb]; fp8: raw 16-byte pieces [rb] (both steps)
   uint4 a[FP8 ? 1 : 2][kMRB];
   uint4 b[2][NQB];
+  // ds_read_b128 operations that fill one Frag
+  static constexpr int na = (FP8 ? 1 : 2) * kMRB;
+  static constexpr int nreads = na + 2 * NQB;
 };
+
+// Read k (0 <= k < nreads) of half u of the stage in ring slot `st`: the A
+// pieces first (step-major), then the B pieces (step-major).
+template <bool FP8, int NQB>
+__device__ __forceinline__ void read_frag_piece(Frag<FP8, NQB> &f, const unsigned char *st,
+                                                int wv, int c, int h, int u, int k) {
+  using G = Geo<FP8>;
+  using F = Frag<FP8, NQB>;
+  if (k < F::na) {
+    const int s = FP8 ? 0 : k / kMRB, rb = k % kMRB;
+    const int slot = FP8 ? swz_slot<G::apieces>(2 * h + u, c)
+                         : swz_slot<G::apieces>(4 * h + 2 * u + s, c);
+    const unsigned char *abase = st + (wv * 32 * kMRB + c) * G::arow;
+    f.a[s][rb] = *reinterpret_cast<const uint4 *>(abase + rb * 32 * G::arow + slot * 16);
+  } else {
+    const int s = (k - F::na) / NQB, qb = (k - F::na) % NQB;
+    const int slot = swz_slot<G::bpieces>(4 * h + 2 * u + s, c);
+    const unsigned char *bbase = st + G::abytes + c * G::brow;
+    f.b[s][qb] = *reinterpret_cast<const uint4 *>(bbase + qb * 32 * G::brow + slot * 16);
+  }
+}
 
 // Read half u of the stage in ring slot `st`.
 template <bool FP8, int NQB>
 __device__ __forceinline__ void read_frags(Frag<FP8, NQB> &f, const unsigned char *st, int wv,
                                            int c, int h, int u) {
-  using G = Geo<FP8>;
-  const unsigned char *abase = st + (wv * 32 * kMRB + c) * G::arow;
-  const unsigned char *bbase = st + G::abytes + c * G::brow;
-  if constexpr (FP8) {
-    const int slot = swz_slot<G::apieces>(2 * h + u, c);
 #pragma unroll
-    for (int rb = 0; rb < kMRB; ++rb)
-      f.a[0][rb] = *reinterpret_cast<const uint4 *>(abase + rb * 32 * G::arow + slot * 16);
-  } else {
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const int slot = swz_slot<G::apieces>(4 * h + 2 * u + s, c);
-#pragma unroll
-      for (int rb = 0; rb < kMRB; ++rb)
-        f.a[s][rb] = *reinterpret_cast<const uint4 *>(abase + rb * 32 * G::arow + slot * 16);
-    }
-  }
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int slot = swz_slot<G::bpieces>(4 * h + 2 * u + s, c);
-#pragma unroll
-    for (int qb = 0; qb < NQB; ++qb)
-      f.b[s][qb] = *reinterpret_cast<const uint4 *>(bbase + qb * 32 * G::brow + slot * 16);
-  }
+  for (int k = 0; k < Frag<FP8, NQB>::nreads; ++k) read_frag_piece<FP8>(f, st, wv, c, h, u, k);
 }
 
 // Redefine the second step's operands of a half stage in place (no code):
@@ -307,6 +314,33 @@ __device__ __forceinline__ void mfma_step(f32x16m (&acc)[kMRB][NQB], const Frag<
     for (int qb = 0; qb < NQB; ++qb)
       acc[rb][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
           av[rb], __builtin_bit_cast(bf16x8m, f.b[s][qb]), ZERO ? zero : acc[rb][qb], 0, 0, 0);
+}
+
+template <bool FP8, bool ZERO, int NOPS, int NQB, typename Op>
+__device__ __forceinline__ void mfma_step_il(f32x16m (&acc)[kMRB][NQB], const Frag<FP8, NQB> &f,
+                                             int s, Op &&op) {
+  bf16x8m av[kMRB];
+#pragma unroll
+  for (int rb = 0; rb < kMRB; ++rb) {
+    if constexpr (FP8) {
+      const uint4 v = f.a[0][rb];
+      if (s == 0) cvt8_fp8_bf16(v.x, v.y, av[rb]);
+      else cvt8_fp8_bf16(v.z, v.w, av[rb]);
+    } else {
+      av[rb] = __builtin_bit_cast(bf16x8m, f.a[s][rb]);
+    }
+  }
+  const f32x16m zero = {};
+  constexpr int NM = kMRB * NQB;
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    const int rb = i / NQB, qb = i % NQB;
+    acc[rb][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+        av[rb], __builtin_bit_cast(bf16x8m, f.b[s][qb]), ZERO ? zero : acc[rb][qb], 0, 0, 0);
+#pragma unroll
+    for (int k = i * NOPS / NM; k < (i + 1) * NOPS / NM; ++k) op(k);
+    __builtin_amdgcn_sched_barrier(0);
+  }
 }
 
 struct MLds {
@@ -813,41 +847,60 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
     // thresholds and row scales, and advances the stream.  issue_a of a
     // chunk always precedes its issue_b.
     int i_tl = 0, i_kc = 0, i_slot = 0, i_sc = 0, i_gt = 0, i_left = T;
-    auto issue_a = [&]() __attribute__((always_inline)) {
-      if (i_left <= 0) return;
+    struct CopyA {
+      i32x4m rs;
+      uint32_t lds, voff;
+    };
+    auto prep_a = [&]() __attribute__((always_inline)) {
+      CopyA ca;
       const int row0 = (t0 + i_tl) * kMNC;
       const int rows = N - row0 < kMNC ? N - row0 : kMNC;
-      const i32x4m ars =
-          make_rsrc((const unsigned char *)a.corpus + (int64_t)row0 * d * G::esz,
-                    (uint32_t)(rows * d * G::esz));
+      ca.rs = make_rsrc((const unsigned char *)a.corpus + (int64_t)row0 * d * G::esz,
+                        (uint32_t)(rows * d * G::esz));
       unsigned char *st = L.ring + i_slot * G::stage;
       const int ln = opaque(lane);
-      // corpus copy j: 1 KiB = (64 / PA) rows of G::arow bytes; lane -> (row,
-      // slot), and the slot receives the piece that the swizzle puts there
       constexpr int PA = G::apieces;
-      const int arow0 = wv * G::adma * (64 / PA) + ln / PA;
-      const uint32_t abase = (uint32_t)(arow0 * d * G::esz +
-                                        swz_slot<PA>(ln % PA, ln / PA) * 16 + i_kc * G::esz);
-#pragma unroll
-      for (int j = 0; j < G::adma; ++j)
-        dma16(ars, st + (wv * G::adma + j) * 1024,
-              abase + (uint32_t)(j * (64 / PA) * d * G::esz));
+      const int wvs = __builtin_amdgcn_readfirstlane(wv);
+      const int arow0 = wvs * G::adma * (64 / PA) + ln / PA;
+      ca.voff = (uint32_t)(arow0 * d * G::esz + swz_slot<PA>(ln % PA, ln / PA) * 16 + i_kc * G::esz);
+      ca.lds = (uint32_t)(uintptr_t)st + wvs * G::adma * 1024;
+      return ca;
     };
-    auto issue_b = [&]() __attribute__((always_inline)) {
+    auto issue_a_j = [&](const CopyA &ca, int j) __attribute__((always_inline)) {
+      constexpr int PA = G::apieces;
+      dma16s(ca.rs, ca.lds + j * 1024, ca.voff + (uint32_t)(j * (64 / PA) * d * G::esz));
+    };
+    auto issue_a = [&]() __attribute__((always_inline)) {
       if (i_left <= 0) return;
-      unsigned char *st = L.ring + i_slot * G::stage;
-      const int ln = opaque(lane);
-      constexpr int PB = G::bpieces;
-      // query copy j: 1 KiB = (64 / PB) rows; pieces past d read as zeros
-      const int bpiece = swz_slot<PB>(ln % PB, ln / PB);
-      const bool bok = i_kc + bpiece * 8 < d;
-      const uint32_t bbase =
-          (uint32_t)(((wv * G::bdma * (64 / PB) + ln / PB) * d + bpiece * 8 + i_kc) * 2);
+      const CopyA ca = prep_a();
 #pragma unroll
-      for (int j = 0; j < G::bdma; ++j) {
-        const uint32_t vo = bok ? bbase + (uint32_t)(j * (64 / PB) * d * 2) : 0x80000000u;
-        dma16(qrs, st + G::abytes + (wv * G::bdma + j) * 1024, vo);
-      }
+      for (int j = 0; j < G::adma; ++j) issue_a_j(ca, j);
+    };
+    struct CopyB {
+      uint32_t lds, voff;
+    };
+    // query part of the next chunk: pieces past d (a partial last stage),
+    // and every piece once the stream has ended, read as zeros through an
+    // offset past the range
+    auto prep_b = [&]() __attribute__((always_inline)) {
+      CopyB cb;
+      constexpr int PB = G::bpieces;
+      const int ln = opaque(lane);
+      const int bpiece = swz_slot<PB>(ln % PB, ln / PB);
+      const int wvs = __builtin_amdgcn_readfirstlane(wv);
+      cb.voff = i_left > 0 && i_kc + bpiece * 8 < d
+                    ? (uint32_t)(((wvs * G::bdma * (64 / PB) + ln / PB) * d + bpiece * 8 + i_kc) * 2)
+                    : 0x80000000u;
+      cb.lds = (uint32_t)(uintptr_t)(L.ring + i_slot * G::stage + G::abytes) + wvs * G::bdma * 1024;
+      return cb;
+    };
+    auto issue_b_j = [&](const CopyB &cb, int j) __attribute__((always_inline)) {
+      constexpr int PB = G::bpieces;
+      dma16s(qrs, cb.lds + j * 1024, cb.voff + (uint32_t)(j * (64 / PB) * d * 2));
+    };
+    auto extras_advance = [&]() __attribute__((always_inline)) {
+      if (i_left <= 0) return;
+      const int ln = opaque(lane);
       if (i_kc == 0) {
         // shared thresholds of the query tile, entries [32 wv, 32 wv + 64)
         const i32x4m grs = make_rsrc(a.gthr + it.qbase, (uint32_t)(it.qvalid * 4));
@@ -875,6 +928,12 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
       }
       i_slot = i_slot + 1 == G::ns ? 0 : i_slot + 1;
       --i_left;
+    };
+    auto issue_b = [&]() __attribute__((always_inline)) {
+      const CopyB cb = prep_b();
+#pragma unroll
+      for (int j = 0; j < G::bdma; ++j) issue_b_j(cb, j);
+      extras_advance();
     };
     // Vector-memory operations issued after the query part of chunk y, up
     // to the corpus part of chunk z (only z's corpus part is issued yet).
@@ -915,26 +974,39 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
     // the LDS reads more than by copy latency.)
     auto stage = [&](auto first_c, bool rd) __attribute__((always_inline)) {
       constexpr bool FIRST = decltype(first_c)::value;
-      mfma_step<FP8, FIRST>(acc, f0, 0);
-      read_frags<FP8>(f1, L.ring + r_slot * G::stage, wv, c, h, 1);
-      if (i_left > 0) {
+      constexpr int NR = Frag<FP8, NQB>::nreads;
+      const unsigned char *cur = L.ring + r_slot * G::stage;
+      const int ln1 = opaque(lane);
+      mfma_step_il<FP8, FIRST, NR>(acc, f0, 0, [&](int k) __attribute__((always_inline)) {
+        read_frag_piece<FP8>(f1, cur, wv, ln1 & 31, ln1 >> 5, 1, k);
+      });
+      {
         __builtin_amdgcn_sched_barrier(0);
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        issue_a();   // this wave's corpus rows of stage g+ns
+        __builtin_amdgcn_sched_barrier(0);
+        CopyA ca = prep_a();   // this wave's corpus rows of stage g+ns
+        if (i_left <= 0) ca.rs.z = 0;
+        mfma_step_il<FP8, false, G::adma>(acc, f0, 1, [&](int k) __attribute__((always_inline)) {
+          issue_a_j(ca, k);
+        });
       }
-      mfma_step<FP8, false>(acc, f0, 1);
       mfma_step<FP8, false>(acc, f1, 0);
       r_slot = r_slot + 1 == G::ns ? 0 : r_slot + 1;
-      if (g + 1 < T) {
-        // stage g+1 landed: younger are the parts of stages g+2 .. g+ns
-        // issued so far
-        wait_vm(younger_ops(g + 1, g + G::ns));
-        bar_lds();
-        issue_b();   // query rows of stage g+ns into the slot stage g used
-      }
+      // stage g+1 landed (after the last stage: all copies landed):
+      // younger are the parts of stages g+2 .. g+ns issued so far
+      wait_vm(younger_ops(g + 1, g + G::ns));
+      bar_lds();
       pin_step1<FP8>(f1);
-      if (rd) read_frags<FP8>(f0, L.ring + r_slot * G::stage, wv, c, h, 0);
-      mfma_step<FP8, false>(acc, f1, 1);
+      const CopyB cb = prep_b();   // query rows of stage g+ns into the slot stage g used
+      const unsigned char *nxt = L.ring + r_slot * G::stage;
+      const int ln0 = opaque(lane);
+      mfma_step_il<FP8, false, G::bdma + NR>(acc, f1, 1, [&](int k) __attribute__((always_inline)) {
+        if (k < G::bdma)
+          issue_b_j(cb, k);
+        else if (rd)
+          read_frag_piece<FP8>(f0, nxt, wv, ln0 & 31, ln0 >> 5, 0, k - G::bdma);
+      });
+      extras_advance();
       ++g;
     };
     // (the first stage of a tile starts the accumulators from zero; its call
