@@ -101,11 +101,14 @@ struct Geo {
   static constexpr int bpieces = brow / 16;
 };
 
-// Slot of 16-byte piece p in a row of P pieces: the 8 rows that fill the 32
-// banks once get distinct slots for the same p.
+// Slot of 16-byte piece p in a row of P pieces.  gfx950's LDS serves a
+// ds_read_b128 16 lanes at a time over 64 banks (256 bytes); the fragment
+// reads have 16 consecutive rows read the same piece, so the 16 / P rows that
+// share a 256-byte window must get distinct slots, for every p: the slot is p
+// XOR the row's window number (mod P).  Only row mod 16 matters.
 template <int P>
 __device__ __forceinline__ int swz_slot(int p, int row) {
-  return p ^ ((row / (8 / P)) & (P - 1));
+  return p ^ ((row / (16 / P)) & (P - 1));
 }
 
 constexpr int kMTail = 16;   // list entries kept in LDS when the lists are global
@@ -849,7 +852,7 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
     int i_tl = 0, i_kc = 0, i_slot = 0, i_sc = 0, i_gt = 0, i_left = T;
     struct CopyA {
       i32x4m rs;
-      uint32_t lds, voff;
+      uint32_t lds, voff, voff1;
     };
     auto prep_a = [&]() __attribute__((always_inline)) {
       CopyA ca;
@@ -863,12 +866,17 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
       const int wvs = __builtin_amdgcn_readfirstlane(wv);
       const int arow0 = wvs * G::adma * (64 / PA) + ln / PA;
       ca.voff = (uint32_t)(arow0 * d * G::esz + swz_slot<PA>(ln % PA, ln / PA) * 16 + i_kc * G::esz);
+      // the swizzle depends on the row mod 16: a bf16 copy holds 8 rows, so odd
+      // copies hold rows 8..15 mod 16 (an fp8 copy holds 16 rows: one pattern)
+      ca.voff1 = (uint32_t)(arow0 * d * G::esz +
+                            swz_slot<PA>(ln % PA, (64 / PA) % 16 + ln / PA) * 16 + i_kc * G::esz);
       ca.lds = (uint32_t)(uintptr_t)st + wvs * G::adma * 1024;
       return ca;
     };
     auto issue_a_j = [&](const CopyA &ca, int j) __attribute__((always_inline)) {
       constexpr int PA = G::apieces;
-      dma16s(ca.rs, ca.lds + j * 1024, ca.voff + (uint32_t)(j * (64 / PA) * d * G::esz));
+      dma16s(ca.rs, ca.lds + j * 1024,
+             ((j & 1) ? ca.voff1 : ca.voff) + (uint32_t)(j * (64 / PA) * d * G::esz));
     };
     auto issue_a = [&]() __attribute__((always_inline)) {
       if (i_left <= 0) return;
@@ -877,7 +885,7 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
       for (int j = 0; j < G::adma; ++j) issue_a_j(ca, j);
     };
     struct CopyB {
-      uint32_t lds, voff;
+      uint32_t lds, voff, voff1;
     };
     // query part of the next chunk: pieces past d (a partial last stage),
     // and every piece once the stream has ended, read as zeros through an
@@ -887,16 +895,20 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
       constexpr int PB = G::bpieces;
       const int ln = opaque(lane);
       const int bpiece = swz_slot<PB>(ln % PB, ln / PB);
+      const int bpiece1 = swz_slot<PB>(ln % PB, 8 + ln / PB);
       const int wvs = __builtin_amdgcn_readfirstlane(wv);
       cb.voff = i_left > 0 && i_kc + bpiece * 8 < d
                     ? (uint32_t)(((wvs * G::bdma * (64 / PB) + ln / PB) * d + bpiece * 8 + i_kc) * 2)
+                    : 0x80000000u;
+      cb.voff1 = i_left > 0 && i_kc + bpiece1 * 8 < d
+                    ? (uint32_t)(((wvs * G::bdma * (64 / PB) + ln / PB) * d + bpiece1 * 8 + i_kc) * 2)
                     : 0x80000000u;
       cb.lds = (uint32_t)(uintptr_t)(L.ring + i_slot * G::stage + G::abytes) + wvs * G::bdma * 1024;
       return cb;
     };
     auto issue_b_j = [&](const CopyB &cb, int j) __attribute__((always_inline)) {
       constexpr int PB = G::bpieces;
-      dma16s(qrs, cb.lds + j * 1024, cb.voff + (uint32_t)(j * (64 / PB) * d * 2));
+      dma16s(qrs, cb.lds + j * 1024, ((j & 1) ? cb.voff1 : cb.voff) + (uint32_t)(j * (64 / PB) * d * 2));
     };
     auto extras_advance = [&]() __attribute__((always_inline)) {
       if (i_left <= 0) return;
