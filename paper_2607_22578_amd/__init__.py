@@ -159,7 +159,8 @@ class Plan:
     desc: hs_merge_desc
 
     def __del__(self):
-        if self.handle:
+        # (at interpreter exit the module's globals may already be gone)
+        if self.handle and _lib is not None:
             _lib.hs_plan_destroy(self.handle)
             self.handle = 0
 
