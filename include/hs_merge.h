@@ -167,6 +167,25 @@ hs_status hs_score_topk(const hs_plan *plan, const void *q_unique, int64_t n_uni
                         const float *row_scale, float *topk_score, int32_t *topk_index,
                         void *ws, size_t ws_bytes, void *stream);
 
+/* hs_score_topk for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same computation and results, with the scratch memory taken from an
+ * array the library holds on each GPU (64 MiB per GPU, allocated with the
+ * library's code object and kept until the process ends) instead of a
+ * workspace argument.  No hipMalloc, hipFree or other allocation happens in
+ * the call.  A plan whose score workspace (what hs_merge_plan reports for the
+ * score step) exceeds 64 MiB is rejected with HS_ERR_WORKSPACE before
+ * anything is enqueued; the 1M-row window (2,048 requests, d = 768, k = 10)
+ * needs about 50 MiB.  Every call on one GPU uses that GPU's one array, which
+ * keeps the previous call's contents (each call writes everything it reads
+ * before reading it): calls that overlap in time on one GPU -- on different
+ * streams, or from host threads without ordering -- race and give wrong
+ * results; order them on one stream.  Arguments as for hs_score_topk. */
+hs_status hs_score_topk_noalloc(const hs_plan *plan, const void *q_unique, int64_t n_unique,
+                                const int64_t *n_unique_dev, const void *corpus,
+                                const float *row_scale, float *topk_score, int32_t *topk_index,
+                                void *stream);
+
 /* Phase 1 of hs_score_topk: scores every distinct query against the corpus in
  * one persistent kernel, each workgroup keeping the k best (score, row) pairs
  * of its corpus slice per query; the per-slice lists go to the workspace

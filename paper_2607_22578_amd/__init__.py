@@ -36,7 +36,8 @@ HS_F32, HS_BF16, HS_FP8_E4M3 = 0, 1, 2
 ABI_VERSION = 2
 
 EXPORTS = ["hs_merge_plan", "hs_plan_destroy", "hs_workflow_rows", "hs_dedup", "hs_score_topk",
-           "hs_score_partial", "hs_topk_merge", "hs_scatter", "hs_deliver", "hs_cache_bytes", "hs_cache_reset", "hs_cache_lookup",
+           "hs_score_topk_noalloc", "hs_score_partial", "hs_topk_merge", "hs_scatter", "hs_deliver",
+           "hs_cache_bytes", "hs_cache_reset", "hs_cache_lookup",
            "hs_cache_insert", "hs_signature", "hs_priority", "hs_status_string",
            "hs_last_error", "hs_abi_version"]
 HS_SIG_NORMALIZE_TEXT = 1
@@ -74,6 +75,8 @@ _lib.hs_dedup.argtypes = [_vp] + [_vp] * 7 + [_vp, _sz, _vp]
 _lib.hs_dedup.restype = ctypes.c_int
 _lib.hs_score_topk.argtypes = [_vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
 _lib.hs_score_topk.restype = ctypes.c_int
+_lib.hs_score_topk_noalloc.argtypes = [_vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp]
+_lib.hs_score_topk_noalloc.restype = ctypes.c_int
 _lib.hs_score_partial.argtypes = [_vp, _vp, _i64, _vp, _vp, _vp, _vp, _sz, _vp]
 _lib.hs_score_partial.restype = ctypes.c_int
 _lib.hs_topk_merge.argtypes = [_vp, _i64, _vp, _vp, _vp, _vp, _sz, _vp]
@@ -224,6 +227,13 @@ def hs_score_topk(plan: Plan, q_unique, n_unique: int, n_unique_dev, corpus, row
     _check(_lib.hs_score_topk(plan.handle, _ptr(q_unique), n_unique, _ptr(n_unique_dev),
                               _ptr(corpus), _ptr(row_scale), _ptr(topk_score), _ptr(topk_index),
                               _ptr(ws), _ws_bytes(ws, ws_bytes), _stream(stream)))
+
+
+def hs_score_topk_noalloc(plan: Plan, q_unique, n_unique: int, n_unique_dev, corpus, row_scale,
+                          topk_score, topk_index, stream=None):
+    _check(_lib.hs_score_topk_noalloc(plan.handle, _ptr(q_unique), n_unique, _ptr(n_unique_dev),
+                                      _ptr(corpus), _ptr(row_scale), _ptr(topk_score),
+                                      _ptr(topk_index), _stream(stream)))
 
 
 def hs_score_partial(plan: Plan, q_unique, n_unique: int, n_unique_dev, corpus, row_scale,

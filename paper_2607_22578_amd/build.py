@@ -10,9 +10,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libhsmerge.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["api.cpp", "cache.hip", "dedup.hip", "gather.hip", "priority.hip", "score.hip",
-           "score_mfma.hip",
-           "signature.hip"]
+SOURCES = ["api.cpp", "cache.hip", "dedup.hip", "gather.hip", "noalloc.hip", "priority.hip",
+           "score.hip", "score_mfma.hip", "signature.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-Wno-unused-function", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

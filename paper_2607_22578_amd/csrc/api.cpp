@@ -24,6 +24,8 @@ hipError_t launch_gather(const void *src, int64_t src_rows, int64_t row_bytes, c
                          hipStream_t st);
 hipError_t launch_deliver(const float *ts, const int32_t *ti, int64_t rows, const int32_t *inv,
                           int64_t R, int k, float *os, int32_t *oi, hipStream_t st);
+size_t noalloc_scratch_bytes();
+hipError_t noalloc_scratch(void **ptr);
 size_t score_workspace_bytes(int64_t cap, int64_t N, int k, int corpus_dtype);
 hipError_t launch_score_partial(const void *q, const void *corpus, const float *scale, int64_t N,
                                 int64_t d, int k, int64_t n_unique, const int64_t *nu_dev,
@@ -312,6 +314,45 @@ hs_status hs_score_topk(const hs_plan *plan, const void *q_unique, int64_t n_uni
   if (s != HS_OK) return s;
   return hs_topk_merge(plan, n_unique, n_unique_dev, topk_score, topk_index, ws, ws_bytes,
                        stream);
+}
+
+hs_status hs_score_topk_noalloc(const hs_plan *plan, const void *q_unique, int64_t n_unique,
+                                const int64_t *n_unique_dev, const void *corpus,
+                                const float *row_scale, float *topk_score, int32_t *topk_index,
+                                void *stream) {
+  if (!plan) return fail(HS_ERR_INVALID_ARG, "hs_score_topk_noalloc: null plan");
+  const size_t cap_bytes = hs::noalloc_scratch_bytes();
+  if (plan->ws_score > cap_bytes)
+    return fail(HS_ERR_WORKSPACE,
+                "hs_score_topk_noalloc: this plan's score step needs %zu bytes of scratch, more "
+                "than the %zu bytes the library holds per GPU (use hs_score_topk with a "
+                "workspace)", plan->ws_score, cap_bytes);
+  // validation of everything but the workspace, before any device call
+  hs_status s = check_nu(plan, n_unique, n_unique_dev, "hs_score_topk_noalloc");
+  if (s != HS_OK) return s;
+  const hs_merge_desc &d = plan->d;
+  if (!q_unique && n_unique != 0)
+    return fail(HS_ERR_INVALID_ARG, "hs_score_topk_noalloc: null q_unique");
+  if (!corpus && d.n_corpus > 0)
+    return fail(HS_ERR_INVALID_ARG, "hs_score_topk_noalloc: null corpus");
+  if (d.corpus_dtype == HS_FP8_E4M3 && d.n_corpus > 0 && !row_scale)
+    return fail(HS_ERR_INVALID_ARG, "hs_score_topk_noalloc: FP8 corpus needs row_scale");
+  if (!aligned(q_unique, 16) || !aligned(corpus, 16) || !aligned(row_scale, 4))
+    return fail(HS_ERR_ALIGNMENT, "hs_score_topk_noalloc: q_unique/corpus must be 16-byte aligned");
+  if ((!topk_score || !topk_index) && n_unique != 0)
+    return fail(HS_ERR_INVALID_ARG, "hs_score_topk_noalloc: null output");
+  if (!aligned(topk_score, 4) || !aligned(topk_index, 4))
+    return fail(HS_ERR_ALIGNMENT, "hs_score_topk_noalloc: misaligned output");
+  void *ws = nullptr;
+  hipError_t e = hs::noalloc_scratch(&ws);
+  if (e != hipSuccess) return device_status(e, "hs_score_topk_noalloc scratch");
+  hipStream_t st = (hipStream_t)stream;
+  e = hs::launch_score_partial(q_unique, corpus, row_scale, d.n_corpus, d.dim, d.k, n_unique,
+                               n_unique_dev, plan->cap, d.corpus_dtype, ws, st);
+  if (e != hipSuccess) return device_status(e, "hs_score_topk_noalloc launch");
+  e = hs::launch_topk_merge(ws, n_unique, n_unique_dev, plan->cap, d.n_corpus, d.k,
+                            d.corpus_dtype, topk_score, topk_index, st);
+  return device_status(e, "hs_score_topk_noalloc launch");
 }
 
 hs_status hs_scatter(const void *src, int64_t src_rows, int64_t row_bytes, const void *index,

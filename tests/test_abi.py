@@ -267,3 +267,19 @@ def test_priority_validation():
     with pytest.raises(hs.HsError) as e:
         hs.hs_priority(p, *args, ws_bytes=16)
     assert e.value.status == hs.HS_ERR_WORKSPACE
+
+
+def test_noalloc_validation():
+    # rejected on the host, before the scratch array is touched
+    big = hs.hs_merge_plan(32768, 1024, 4_000_000, 32, hs.HS_BF16, hs.HS_BF16)
+    with pytest.raises(hs.HsError) as e:
+        hs.hs_score_topk_noalloc(big, FAKE, 10, None, FAKE, None, FAKE, FAKE)
+    assert e.value.status == hs.HS_ERR_WORKSPACE and "scratch" in hs.hs_last_error()
+    p = hs.hs_merge_plan(**GOOD)
+    for args, code in [((FAKE, 4096, None, FAKE, None, FAKE, FAKE), hs.HS_ERR_INVALID_ARG),
+                       ((FAKE, -1, None, FAKE, None, FAKE, FAKE), hs.HS_ERR_INVALID_ARG),
+                       ((FAKE, 10, None, FAKE + 2, None, FAKE, FAKE), hs.HS_ERR_ALIGNMENT),
+                       ((FAKE, 10, None, FAKE, None, None, FAKE), hs.HS_ERR_INVALID_ARG)]:
+        with pytest.raises(hs.HsError) as e:
+            hs.hs_score_topk_noalloc(p, *args)
+        assert e.value.status == code, args
