@@ -4,7 +4,7 @@
 // Every entry point validates all of its arguments before it enqueues
 // anything, so a non-OK status means nothing was launched and no output was
 // touched.  No entry point allocates device memory.
-#include <hip/hip_runtime.h>
+#include <hip/hip_runtime_api.h>
 
 #include <cmath>
 #include <cstdarg>
