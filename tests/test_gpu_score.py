@@ -65,6 +65,26 @@ def test_fp32_k_values(k):
     check_delivery(m, cfg_w.R)
 
 
+@pytest.mark.parametrize("d", [4, 36, 96, 100])
+@pytest.mark.parametrize("k", [10, 40])
+def test_fp32_odd_widths(d, k):
+    # widths whose 32-wide K chunks are odd in number (d = 96: three) or end in
+    # a partial chunk (d = 4, 36, 100), so the two-ahead K prefetch takes its
+    # mid-loop exit and its zero-filled last chunk; k <= 32 (one wave per query
+    # ranks a tile with its list) and k > 32 (lists in the workspace); a ragged
+    # corpus of 2,999 rows (the last 64-row tile partial)
+    cfg_w = synth.make("ridge1m", n_corpus=1, with_corpus=False)
+    ids = cfg_w.template_ids[:300]
+    keys = cfg_w.keys[:300]
+    q, _ = synth.gaussian_rows(cfg_w.seed, synth.S_QUERY, 0, d, "f32", row_ids=ids)
+    c, _ = synth.gaussian_rows(cfg_w.seed, synth.S_CORPUS, 2_999, d, "f32")
+    note(f"fp32 d={d} k={k}")
+    m = run_merge(keys, q, c, k)
+    ref = check_dedup(m, keys)
+    check_unique_topk(m, ref, q, c, k)
+    check_delivery(m, len(keys))
+
+
 @pytest.mark.parametrize("k", [1, 32, 100])
 def test_k_values(k):
     w = synth.make("ridge1m", n_corpus=9_000)
