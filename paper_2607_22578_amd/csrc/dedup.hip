@@ -15,11 +15,12 @@
 //                    group through the table;
 //   R <= kSmallMax : one workgroup sorts (key, idx) in LDS with a bitonic
 //                    network and compacts in the same launch;
-//   larger R       : LSD radix sort, 8-bit digits over (key - min) so only
-//                    the bits that vary are sorted (the pass count is read on
-//                    the device; surplus passes exit at once), stable local
-//                    ranking with wavefront ballots, then head flags, a
-//                    block-prefix compaction and a counts pass.
+//   larger R       : the key range is found on the device; keys that take at
+//                    most R values are grouped by direct addressing over the
+//                    range, others by an LSD radix sort (8-bit digits over
+//                    key - min, so only the bits that vary are sorted; stable
+//                    local ranking with wavefront ballots, then head flags, a
+//                    compaction and group sizes) in one persistent launch.
 #include "common.h"
 
 namespace hs {
@@ -260,32 +261,127 @@ __global__ __launch_bounds__(kSmallThreads) void dedup_hash_kernel(
   if (tid == 0) *nu_out = (int64_t)n;
 }
 
-// ---------------------------------------------------------------- radix path
+// ---------------------------------------------------------------- larger R
+//
+// Five launches whatever the keys:
+//   prep    : mapped keys and request numbers, per-workgroup key min/max, and
+//             the scratch the later launches need at its neutral value;
+//   mark    : every workgroup reduces the min/max itself and picks the path;
+//             dense path (the keys take at most R values, max - min < R):
+//             first request and group size per key value;
+//   groups  : dense path: the present values numbered in ascending order by
+//             a single-pass scan (each value block looks back at the running
+//             totals of the blocks before it), with the per-group outputs;
+//   inverse : dense path: request -> group;
+//   radix   : sort path (returns at once on the dense path): one persistent
+//             launch of at most kRadixGridMax workgroups, all resident, that
+//             runs every LSD pass (8-bit digits of key - min, one pass per
+//             8 bits of max - min), then head flags, compaction and group
+//             sizes, with grid barriers between the phases.
+// The three dense launches return at once on the sort path.
+
+constexpr int kPrepMax = 1024;        // prep workgroups (min/max partials)
+constexpr int kRadixGridMax = 256;    // workgroups of the persistent sort
+constexpr int kBarGroups = 16;        // arrival counters of the grid barrier
+constexpr int kCtlStride = 32;        // 32-bit words between counters (128 B)
+// control words: [0] value-block ticket of the groups launch; barrier
+// arrival counter j at (1 + j) * kCtlStride; the barrier's release counter at
+// (1 + kBarGroups) * kCtlStride
+constexpr int kCtlWords = (2 + kBarGroups) * kCtlStride;
 
 struct RadixWs {
   uint64_t *keyA, *keyB;
   int32_t *idxA, *idxB;
-  uint64_t *pmin, *pmax;   // per-block min/max of mapped keys
+  uint64_t *pmin, *pmax;   // per-prep-workgroup min/max of mapped keys
   uint64_t *range;         // [0] = global min, [1] = radix pass count,
                            // [2] = key values of the dense path (0: radix)
-  uint32_t *hist;          // kBins x nb, digit-major
-  uint32_t *bheads;        // heads per block
+  uint32_t *hist;          // kBins x nb, digit-major (scanned in place)
+  uint32_t *dtot;          // kBins digit totals of a pass
+  uint32_t *bheads;        // heads per tile (scanned in place)
   int32_t *start;          // group start positions
+  uint64_t *flags;         // dense value blocks: running-total words
+  uint32_t *ctl;           // kCtlWords control words
 };
 
-__global__ __launch_bounds__(kRadixThreads) void radix_prep_kernel(
+// ------------------------------------------------ grid-wide helpers
+
+// Barrier over the G workgroups of a launch that are all resident at once
+// (G at most what the device holds of them).  `k`
+// counts the barriers this workgroup has passed (the counters only grow
+// within a launch; prep zeroes them).  Arrivals are spread over kBarGroups
+// counters so that no single address takes all G of them; the last arrival
+// of each group bumps the release counter that everyone waits on.
+__device__ __forceinline__ void grid_barrier(uint32_t *ctl, int G, uint32_t &k) {
+  ++k;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int ng = G < kBarGroups ? G : kBarGroups;
+    const int j = (int)blockIdx.x % ng;
+    const uint32_t gsize = (uint32_t)(G / ng + (j < G % ng ? 1 : 0));
+    uint32_t *sub = ctl + (1 + j) * kCtlStride;
+    uint32_t *rel = ctl + (1 + kBarGroups) * kCtlStride;
+    const uint32_t old =
+        __hip_atomic_fetch_add(sub, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    if (old + 1 == k * gsize)
+      __hip_atomic_fetch_add(rel, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    while (__hip_atomic_load(rel, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < k * (uint32_t)ng)
+      __builtin_amdgcn_s_sleep(1);
+  }
+  __syncthreads();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
+
+// Exclusive prefix sum of a[0, n) in place by one workgroup; returns the
+// total.
+__device__ uint32_t block_scan_inplace(uint32_t *a, int64_t n) {
+  __shared__ uint32_t wsum[kRadixThreads / 64 + 1];
+  constexpr int P = 4;
+  uint32_t carry = 0;
+  for (int64_t c0 = 0; c0 < n; c0 += kRadixThreads * P) {
+    const int64_t i0 = c0 + (int64_t)threadIdx.x * P;
+    uint32_t v[P], sum = 0;
+#pragma unroll
+    for (int e = 0; e < P; ++e) {
+      v[e] = i0 + e < n ? a[i0 + e] : 0u;
+      sum += v[e];
+    }
+    uint32_t total;
+    uint32_t run = carry + block_inclusive_scan<kRadixThreads>(sum, wsum, total) - sum;
+#pragma unroll
+    for (int e = 0; e < P; ++e)
+      if (i0 + e < n) {
+        a[i0 + e] = run;
+        run += v[e];
+      }
+    carry += total;
+  }
+  return carry;
+}
+
+// ------------------------------------------------ prep and path choice
+
+// Workgroup b of P: chunks of kPrepChunk requests b, b + P, ... -> mapped
+// keys (keyA), request numbers (idxA) and the min/max over them; the dense
+// tables for up to R values, the value-block words and the control words to
+// their neutral values.
+constexpr int kPrepChunk = 4 * kRadixThreads;
+__global__ __launch_bounds__(kRadixThreads) void dedup_prep_kernel(
     const int64_t *__restrict__ keys, int R, RadixWs ws) {
   __shared__ uint64_t smin[kRadixThreads / 64], smax[kRadixThreads / 64];
-  const int b = blockIdx.x, tid = threadIdx.x;
+  const int tid = threadIdx.x, P = gridDim.x;
   uint64_t mn = ~0ull, mx = 0ull;
-  for (int e = 0; e < kRadixItems; ++e) {
-    int p = b * kTile + e * kRadixThreads + tid;
-    if (p < R) {
-      uint64_t k = map_key(keys[p]);
-      ws.keyA[p] = k;
-      ws.idxA[p] = p;
-      mn = k < mn ? k : mn;
-      mx = k > mx ? k : mx;
+  for (int64_t c = blockIdx.x; c * kPrepChunk < R; c += P) {
+#pragma unroll
+    for (int e = 0; e < kPrepChunk / kRadixThreads; ++e) {
+      const int64_t p = c * kPrepChunk + e * kRadixThreads + tid;
+      if (p < R) {
+        const uint64_t k = map_key(keys[p]);
+        ws.keyA[p] = k;
+        ws.idxA[p] = (int32_t)p;
+        mn = k < mn ? k : mn;
+        mx = k > mx ? k : mx;
+      }
     }
   }
   for (int o = 32; o > 0; o >>= 1) {
@@ -303,16 +399,38 @@ __global__ __launch_bounds__(kRadixThreads) void radix_prep_kernel(
       mn = smin[w] < mn ? smin[w] : mn;
       mx = smax[w] > mx ? smax[w] : mx;
     }
-    ws.pmin[b] = mn;
-    ws.pmax[b] = mx;
+    ws.pmin[blockIdx.x] = mn;
+    ws.pmax[blockIdx.x] = mx;
   }
+  // dense tables (first request, group size) over [0, R) >= [0, nv)
+  int32_t *first = (int32_t *)ws.keyB, *count = (int32_t *)ws.keyB + R;
+  const int64_t gt = (int64_t)blockIdx.x * kRadixThreads + tid;
+  const int64_t gs = (int64_t)P * kRadixThreads;
+  for (int64_t v = gt; v < R; v += gs) {
+    first[v] = 0x7fffffff;
+    count[v] = 0;
+  }
+  const int64_t nvb = ((int64_t)R + 1023) / 1024;
+  for (int64_t i = gt; i < nvb; i += gs) ws.flags[i] = 0ull;
+  if (blockIdx.x == 0)
+    for (int i = tid; i < kCtlWords; i += kRadixThreads) ws.ctl[i] = 0u;
 }
 
-__global__ __launch_bounds__(1024) void radix_range_kernel(int R, int nb, RadixWs ws) {
-  __shared__ uint64_t smin[16], smax[16];
+struct Range {
+  uint64_t mn;
+  uint64_t npass;   // radix passes (0 on the dense path)
+  uint64_t nv;      // key values of the dense path (0: radix path)
+};
+
+// Global min/max over the P prep partials and the path: dense when the keys
+// take at most R values (max - min < R), else radix with one pass per 8 bits
+// of max - min.  Computed by every workgroup that calls it.
+__device__ Range range_of(int R, int P, const RadixWs &ws) {
+  __shared__ uint64_t smin[kRadixThreads / 64], smax[kRadixThreads / 64];
+  __shared__ Range res;
   const int tid = threadIdx.x;
   uint64_t mn = ~0ull, mx = 0ull;
-  for (int i = tid; i < nb; i += 1024) {
+  for (int i = tid; i < P; i += kRadixThreads) {
     mn = ws.pmin[i] < mn ? ws.pmin[i] : mn;
     mx = ws.pmax[i] > mx ? ws.pmax[i] : mx;
   }
@@ -327,32 +445,193 @@ __global__ __launch_bounds__(1024) void radix_range_kernel(int R, int nb, RadixW
   }
   __syncthreads();
   if (tid == 0) {
-    for (int w = 1; w < 16; ++w) {
+    for (int w = 1; w < kRadixThreads / 64; ++w) {
       mn = smin[w] < mn ? smin[w] : mn;
       mx = smax[w] > mx ? smax[w] : mx;
     }
-    uint64_t span = mx - mn;
-    int bits = span ? 64 - __clzll((long long)span) : 0;
-    // dense path when the keys take at most R values
+    const uint64_t span = mx - mn;
+    const int bits = span ? 64 - __clzll((long long)span) : 0;
     const bool dense = span < (uint64_t)R;
-    ws.range[0] = mn;
-    ws.range[1] = dense ? 0ull : (uint64_t)((bits + kRadixBits - 1) / kRadixBits);
-    ws.range[2] = dense ? span + 1 : 0ull;
+    res.mn = mn;
+    res.npass = dense ? 0ull : (uint64_t)((bits + kRadixBits - 1) / kRadixBits);
+    res.nv = dense ? span + 1 : 0ull;
+  }
+  __syncthreads();
+  return res;
+}
+
+// ---------------------------------------------------------------- dense path
+//
+// When the R mapped keys take at most R values (e.g. chunk row ids), the
+// groups are found by direct addressing over [min, max] instead of sorting:
+// per key value v, the first request (atomic min) and the group size (atomic
+// add); a scan over the values numbers the present ones in ascending key
+// order; each request then reads its group.  Same canonical outputs as the
+// sort.  Value arrays reuse the sort's second buffers: first/count in keyB
+// (2 x int32 per value), group ids in idxB.
+
+constexpr int kDenseBlk = 1024;                        // values per value block
+constexpr int kDensePer = kDenseBlk / kRadixThreads;   // values per thread
+constexpr int kAggRound = 1024, kAggSlots = 2048;
+
+// Rounds of kAggRound consecutive requests are first combined per key value
+// in an LDS table (a hot key appears many times per round), then each table
+// entry goes to the value arrays with one atomic min and one atomic add.
+// Workgroup 0 also stores the path for the later launches.
+__global__ __launch_bounds__(kRadixThreads) void dense_mark_kernel(int R, int P, RadixWs ws) {
+  __shared__ int32_t tkey[kAggSlots];
+  __shared__ int32_t tfirst[kAggSlots];
+  __shared__ int32_t tcount[kAggSlots];
+  const Range rg = range_of(R, P, ws);
+  const int tid = threadIdx.x;
+  if (blockIdx.x == 0 && tid == 0) {
+    ws.range[0] = rg.mn;
+    ws.range[1] = rg.npass;
+    ws.range[2] = rg.nv;
+  }
+  if (!rg.nv) return;
+  int32_t *first = (int32_t *)ws.keyB, *count = (int32_t *)ws.keyB + R;
+  for (int64_t round = blockIdx.x; round * kAggRound < R; round += gridDim.x) {
+    const int64_t base = round * kAggRound;
+    for (int j = tid; j < kAggSlots; j += kRadixThreads) {
+      tkey[j] = -1;
+      tfirst[j] = 0x7fffffff;
+      tcount[j] = 0;
+    }
+    __syncthreads();
+    for (int j = tid; j < kAggRound; j += kRadixThreads) {
+      const int64_t p = base + j;
+      if (p >= R) break;
+      const int32_t v = (int32_t)(ws.keyA[p] - rg.mn);   // < nv <= R
+      uint32_t h = ((uint32_t)v * 2654435761u) & (kAggSlots - 1);
+      for (;;) {   // at most kAggRound keys in kAggSlots slots: a slot is found
+        const int32_t prev = atomicCAS(&tkey[h], -1, v);
+        if (prev == -1 || prev == v) break;
+        h = (h + 1) & (kAggSlots - 1);
+      }
+      atomicMin(&tfirst[h], (int32_t)p);
+      atomicAdd(&tcount[h], 1);
+    }
+    __syncthreads();
+    for (int j = tid; j < kAggSlots; j += kRadixThreads) {
+      const int32_t v = tkey[j];
+      if (v >= 0) {
+        atomicMin(&first[v], tfirst[j]);
+        atomicAdd(&count[v], tcount[j]);
+      }
+    }
+    __syncthreads();
   }
 }
+
+// Value-block words: state in the high half (1: the block's own count, 2:
+// the running total through the block), the number in the low half.
+constexpr uint64_t kFlagAgg = 1ull << 32, kFlagPrefix = 2ull << 32;
+
+// One value block per workgroup, in the order the workgroups start (a ticket,
+// so every block it waits on has started): count the present values, publish
+// the count, add up the counts or running totals of the blocks before it,
+// publish the running total, then number its present values and write the
+// per-group outputs.  The last block writes n_u.
+__global__ __launch_bounds__(kRadixThreads) void dense_groups_kernel(
+    int R, RadixWs ws, int64_t *__restrict__ uk, int32_t *__restrict__ fi,
+    int32_t *__restrict__ cnt, int64_t *__restrict__ nu_out) {
+  __shared__ uint32_t wsum[kRadixThreads / 64 + 1];
+  __shared__ uint32_t s_vb, s_before;
+  const uint64_t nv = ws.range[2];
+  const uint64_t nvb = (nv + kDenseBlk - 1) / kDenseBlk;
+  if (!nv || blockIdx.x >= nvb) return;
+  const int tid = threadIdx.x;
+  if (tid == 0)
+    s_vb = __hip_atomic_fetch_add(ws.ctl, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  const uint64_t vb = s_vb;
+  const uint64_t mn = ws.range[0];
+  const int32_t *first = (const int32_t *)ws.keyB, *count = (const int32_t *)ws.keyB + R;
+  int32_t *gid = ws.idxB;
+  const uint64_t v0 = vb * kDenseBlk + (uint64_t)tid * kDensePer;
+  int32_t c[kDensePer];
+  uint32_t pr = 0;
+#pragma unroll
+  for (int e = 0; e < kDensePer; ++e) {
+    c[e] = v0 + e < nv ? count[v0 + e] : 0;
+    pr += c[e] > 0 ? 1u : 0u;
+  }
+  uint32_t total;
+  const uint32_t incl = block_inclusive_scan<kRadixThreads>(pr, wsum, total);
+  if (tid < 64) {
+    // wave 0: publish this block's count, then add up the words of the
+    // blocks before it, 64 at a time, back to the nearest running total
+    // (blocks before the first count as a running total of 0)
+    uint64_t *fl = ws.flags;
+    const int lane = tid;
+    uint32_t before = 0;
+    if (vb == 0) {
+      if (lane == 0)
+        __hip_atomic_store(&fl[0], kFlagPrefix | total, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      if (lane == 0)
+        __hip_atomic_store(&fl[vb], kFlagAgg | total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int64_t j0 = (int64_t)vb - 1;; j0 -= 64) {
+        const int64_t j = j0 - lane;
+        uint64_t f = j >= 0 ? __hip_atomic_load(&fl[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                            : kFlagPrefix;
+        while (__any(f == 0ull)) {
+          __builtin_amdgcn_s_sleep(1);
+          if (f == 0ull) f = __hip_atomic_load(&fl[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        const uint64_t pm = __ballot(f >= kFlagPrefix);
+        const int stop = pm ? __ffsll((long long)pm) - 1 : 64;
+        uint32_t v = lane <= stop ? (uint32_t)f : 0u;
+        for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+        before += v;
+        if (pm) break;
+      }
+      if (lane == 0)
+        __hip_atomic_store(&fl[vb], kFlagPrefix | (before + total), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (lane == 0) s_before = before;
+  }
+  __syncthreads();
+  uint32_t g = s_before + incl - pr;
+#pragma unroll
+  for (int e = 0; e < kDensePer; ++e) {
+    const uint64_t v = v0 + e;
+    if (c[e] > 0) {
+      uk[g] = unmap_key(mn + v);
+      fi[g] = first[v];
+      if (cnt) cnt[g] = c[e];
+      gid[v] = (int32_t)g;
+      ++g;
+    }
+  }
+  if (vb + 1 == nvb && tid == 0) *nu_out = (int64_t)(s_before + total);
+}
+
+// Request -> group.
+__global__ __launch_bounds__(256) void dense_inverse_kernel(int R, RadixWs ws,
+                                                            int32_t *__restrict__ inv) {
+  const uint64_t nv = ws.range[2];
+  if (!nv) return;
+  const uint64_t mn = ws.range[0];
+  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < R; p += (int64_t)gridDim.x * 256)
+    inv[p] = ws.idxB[ws.keyA[p] - mn];
+}
+
+// ---------------------------------------------------------------- sort path
 
 __device__ __forceinline__ uint32_t digit_of(uint64_t k, uint64_t mn, int pass) {
   return (uint32_t)(((k - mn) >> (pass * kRadixBits)) & (kBins - 1));
 }
 
-__global__ __launch_bounds__(kRadixThreads) void radix_hist_kernel(int R, int nb, int pass,
-                                                                   RadixWs ws) {
+// Digit histogram of tile b for one pass.
+__device__ __forceinline__ void hist_phase(int R, int nb, int pass, uint64_t mn, int b,
+                                           const RadixWs &ws) {
   __shared__ uint32_t h[kBins];
-  const uint64_t npass = ws.range[1];
-  if ((uint64_t)pass >= npass) return;
-  const uint64_t mn = ws.range[0];
   const uint64_t *src = (pass & 1) ? ws.keyB : ws.keyA;
-  const int b = blockIdx.x, tid = threadIdx.x;
+  const int tid = threadIdx.x;
   h[tid] = 0;
   __syncthreads();
   for (int e = 0; e < kRadixItems; ++e) {
@@ -361,33 +640,43 @@ __global__ __launch_bounds__(kRadixThreads) void radix_hist_kernel(int R, int nb
   }
   __syncthreads();
   ws.hist[tid * nb + b] = h[tid];
+  __syncthreads();
 }
 
-__global__ __launch_bounds__(kRadixThreads) void radix_scatter_kernel(int R, int nb, int pass,
-                                                                      RadixWs ws) {
+// Stable scatter of tile b by its digit for one pass.  With at most
+// kDirectTiles tiles the digit offsets come straight from the histogram;
+// otherwise its rows are already exclusive scans over the tiles and dtot
+// holds the digit totals.
+constexpr int kDirectTiles = 64;
+__device__ __forceinline__ void scatter_phase(int R, int nb, int pass, uint64_t mn, int b,
+                                              const RadixWs &ws) {
   __shared__ uint32_t goff[kBins];
   __shared__ uint32_t running[kBins];
   __shared__ uint32_t wcount[kRadixThreads / 64][kBins];
   __shared__ uint32_t wsum[kRadixThreads / 64 + 1];
-  const uint64_t npass = ws.range[1];
-  if ((uint64_t)pass >= npass) return;
-  const uint64_t mn = ws.range[0];
   const uint64_t *ksrc = (pass & 1) ? ws.keyB : ws.keyA;
   uint64_t *kdst = (pass & 1) ? ws.keyA : ws.keyB;
   const int32_t *isrc = (pass & 1) ? ws.idxB : ws.idxA;
   int32_t *idst = (pass & 1) ? ws.idxA : ws.idxB;
-  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
 
-  // global base of each digit for this block: all smaller digits everywhere,
-  // plus this digit in earlier blocks
-  uint32_t tot = 0, prior = 0;
-  for (int bb = 0; bb < nb; ++bb) {
-    uint32_t c = ws.hist[tid * nb + bb];
-    tot += c;
-    if (bb < b) prior += c;
+  // global base of each digit for this tile: all smaller digits everywhere,
+  // plus this digit in earlier tiles
+  uint32_t tot, prior;
+  if (nb <= kDirectTiles) {
+    tot = 0;
+    prior = 0;
+    for (int bb = 0; bb < nb; ++bb) {
+      const uint32_t c = ws.hist[tid * nb + bb];
+      tot += c;
+      prior += bb < b ? c : 0u;
+    }
+  } else {
+    tot = ws.dtot[tid];
+    prior = ws.hist[tid * nb + b];
   }
   uint32_t total;
-  uint32_t incl = block_inclusive_scan<kRadixThreads>(tot, wsum, total);
+  const uint32_t incl = block_inclusive_scan<kRadixThreads>(tot, wsum, total);
   goff[tid] = incl - tot + prior;
   running[tid] = 0;
   const uint64_t lt = (1ull << lane) - 1ull;
@@ -426,18 +715,18 @@ __global__ __launch_bounds__(kRadixThreads) void radix_scatter_kernel(int R, int
   }
 }
 
-__device__ __forceinline__ const uint64_t *sorted_keys(const RadixWs &ws) {
-  return (ws.range[1] & 1) ? ws.keyB : ws.keyA;
+__device__ __forceinline__ const uint64_t *sorted_keys(const RadixWs &ws, uint64_t npass) {
+  return (npass & 1) ? ws.keyB : ws.keyA;
 }
-__device__ __forceinline__ const int32_t *sorted_idx(const RadixWs &ws) {
-  return (ws.range[1] & 1) ? ws.idxB : ws.idxA;
+__device__ __forceinline__ const int32_t *sorted_idx(const RadixWs &ws, uint64_t npass) {
+  return (npass & 1) ? ws.idxB : ws.idxA;
 }
 
-__global__ __launch_bounds__(kRadixThreads) void radix_heads_kernel(int R, RadixWs ws) {
+// Group heads (first of each run of equal keys) in tile b of the sorted keys.
+__device__ __forceinline__ void heads_phase(int R, uint64_t npass, int b, const RadixWs &ws) {
   __shared__ uint32_t wsum[kRadixThreads / 64 + 1];
-  if (ws.range[2]) return;   // dense path
-  const uint64_t *k = sorted_keys(ws);
-  const int b = blockIdx.x, tid = threadIdx.x;
+  const uint64_t *k = sorted_keys(ws, npass);
+  const int tid = threadIdx.x;
   uint32_t h = 0;
   for (int e = 0; e < kRadixItems; ++e) {
     int p = b * kTile + e * kRadixThreads + tid;
@@ -448,18 +737,17 @@ __global__ __launch_bounds__(kRadixThreads) void radix_heads_kernel(int R, Radix
   if (tid == 0) ws.bheads[b] = total;
 }
 
-__global__ __launch_bounds__(kRadixThreads) void radix_compact_kernel(
-    int R, RadixWs ws, int64_t *__restrict__ uk, int32_t *__restrict__ fi,
-    int32_t *__restrict__ inv, int64_t *__restrict__ nu_out) {
+// Distinct keys, survivors and the request -> group map from tile b; bheads
+// holds the heads before each tile.
+__device__ __forceinline__ void compact_phase(int R, uint64_t npass, int b, const RadixWs &ws,
+                                              int64_t *__restrict__ uk, int32_t *__restrict__ fi,
+                                              int32_t *__restrict__ inv,
+                                              int64_t *__restrict__ nu_out) {
   __shared__ uint32_t wsum[kRadixThreads / 64 + 1];
-  if (ws.range[2]) return;   // dense path
-  const uint64_t *k = sorted_keys(ws);
-  const int32_t *ix = sorted_idx(ws);
-  const int b = blockIdx.x, tid = threadIdx.x;
-  uint32_t before = 0;
-  for (int bb = tid; bb < b; bb += kRadixThreads) before += ws.bheads[bb];
-  uint32_t g0;  // heads in all earlier blocks
-  block_inclusive_scan<kRadixThreads>(before, wsum, g0);
+  const uint64_t *k = sorted_keys(ws, npass);
+  const int32_t *ix = sorted_idx(ws, npass);
+  const int tid = threadIdx.x;
+  const uint32_t g0 = ws.bheads[b];
   // thread t owns positions [base + t*I, base + t*I + I) so that the scan
   // order is the sorted order
   const int base = b * kTile + tid * kRadixItems;
@@ -492,138 +780,73 @@ __global__ __launch_bounds__(kRadixThreads) void radix_compact_kernel(
   }
 }
 
-__global__ __launch_bounds__(256) void radix_counts_kernel(int R, RadixWs ws,
-                                                           const int64_t *__restrict__ nu,
-                                                           int32_t *__restrict__ cnt) {
+// The whole sort path in one persistent launch of G workgroups (all resident
+// at once): per pass a
+// digit histogram per tile, with more than kDirectTiles tiles an exclusive
+// scan of each digit's row over the tiles (rows spread over the wavefronts),
+// and the stable scatter; then
+// head counts per tile, their scan (workgroup 0), the compaction and the
+// group sizes.  Tiles are taken b, b + G, ...; the barrier count is the same
+// for every workgroup.
+__global__ __launch_bounds__(kRadixThreads) void radix_sort_kernel(
+    int R, int nb, RadixWs ws, int64_t *__restrict__ uk, int32_t *__restrict__ fi,
+    int32_t *__restrict__ cnt, int32_t *__restrict__ inv, int64_t *__restrict__ nu_out) {
   if (ws.range[2]) return;   // dense path
-  int g = blockIdx.x * 256 + threadIdx.x;
-  if (g < R && (int64_t)g < *nu) cnt[g] = ws.start[g + 1] - ws.start[g];
-}
-
-// ---------------------------------------------------------------- dense path
-//
-// When the R mapped keys take at most R values (max - min < R: e.g. chunk
-// row ids), the groups are found by direct addressing over [min, max]
-// instead of sorting: per key value v, the first request (atomic min) and the
-// group size (atomic add); a scan over the values numbers the present ones
-// in ascending key order; each request then reads its group.  Same canonical
-// outputs as the sort.  Value arrays reuse the sort's second buffers:
-// first/count in keyB (2 x int32 per value), group ids in idxB; the scan's
-// block sums use the histogram buffer.
-
-constexpr int kDenseBlk = 1024;                  // values per scan block
-constexpr int kAggRound = 1024, kAggSlots = 2048;
-
-__device__ __forceinline__ int32_t *dense_first(const RadixWs &ws) { return (int32_t *)ws.keyB; }
-__device__ __forceinline__ int32_t *dense_count(const RadixWs &ws, uint64_t nv) {
-  return (int32_t *)ws.keyB + nv;
-}
-
-__global__ void dense_clear_kernel(RadixWs ws) {
-  const uint64_t nv = ws.range[2];
-  if (!nv) return;
-  int32_t *first = dense_first(ws), *count = dense_count(ws, nv);
-  for (uint64_t v = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; v < nv;
-       v += (uint64_t)gridDim.x * blockDim.x) {
-    first[v] = 0x7fffffff;
-    count[v] = 0;
-  }
-}
-
-// Rounds of kAggRound consecutive requests are first combined per key value
-// in an LDS table (a hot key appears many times per round), then each table
-// entry goes to the value arrays with one atomic min and one atomic add.
-__global__ __launch_bounds__(256) void dense_mark_kernel(int R, RadixWs ws) {
-  __shared__ int32_t tkey[kAggSlots];
-  __shared__ int32_t tfirst[kAggSlots];
-  __shared__ int32_t tcount[kAggSlots];
-  const uint64_t nv = ws.range[2];
-  if (!nv) return;
-  const uint64_t mn = ws.range[0];
-  int32_t *first = dense_first(ws), *count = dense_count(ws, nv);
-  const int tid = threadIdx.x;
-  for (int64_t r0 = (int64_t)blockIdx.x * kAggRound; r0 < R;
-       r0 += (int64_t)gridDim.x * kAggRound) {
-    for (int j = tid; j < kAggSlots; j += 256) {
-      tkey[j] = -1;
-      tfirst[j] = 0x7fffffff;
-      tcount[j] = 0;
-    }
-    __syncthreads();
-    for (int j = tid; j < kAggRound; j += 256) {
-      const int64_t p = r0 + j;
-      if (p >= R) break;
-      const int32_t v = (int32_t)(ws.keyA[p] - mn);   // < nv <= R
-      uint32_t h = ((uint32_t)v * 2654435761u) & (kAggSlots - 1);
-      for (;;) {   // at most kAggRound keys in kAggSlots slots: a slot is found
-        const int32_t prev = atomicCAS(&tkey[h], -1, v);
-        if (prev == -1 || prev == v) break;
-        h = (h + 1) & (kAggSlots - 1);
+  const uint64_t mn = ws.range[0], npass = ws.range[1];
+  const int G = gridDim.x, b = blockIdx.x;
+  uint32_t k = 0;
+  const int wid = b * (kRadixThreads / 64) + (threadIdx.x >> 6), nw = G * (kRadixThreads / 64);
+  const int lane = threadIdx.x & 63;
+  for (int pass = 0; pass < (int)npass; ++pass) {
+    for (int t = b; t < nb; t += G) hist_phase(R, nb, pass, mn, t, ws);
+    grid_barrier(ws.ctl, G, k);
+    if (nb > kDirectTiles) {
+      // each digit's row: exclusive scan over the tiles by one wavefront
+      for (int d = wid; d < kBins; d += nw) {
+        uint32_t *row = ws.hist + (int64_t)d * nb;
+        uint32_t carry = 0;
+        for (int c0 = 0; c0 < nb; c0 += 4 * 64) {
+          const int i0 = c0 + lane * 4;
+          uint32_t v[4], sum = 0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[e] = i0 + e < nb ? row[i0 + e] : 0u;
+            sum += v[e];
+          }
+          uint32_t x = sum;
+#pragma unroll
+          for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t y = __shfl_up(x, o, 64);
+            if (lane >= o) x += y;
+          }
+          uint32_t run = carry + x - sum;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (i0 + e < nb) {
+              row[i0 + e] = run;
+              run += v[e];
+            }
+          carry += __shfl(x, 63, 64);
+        }
+        if (lane == 0) ws.dtot[d] = carry;
       }
-      atomicMin(&tfirst[h], (int32_t)p);
-      atomicAdd(&tcount[h], 1);
+      grid_barrier(ws.ctl, G, k);
     }
-    __syncthreads();
-    for (int j = tid; j < kAggSlots; j += 256) {
-      const int32_t v = tkey[j];
-      if (v >= 0) {
-        atomicMin(&first[v], tfirst[j]);
-        atomicAdd(&count[v], tcount[j]);
-      }
-    }
-    __syncthreads();
+    for (int t = b; t < nb; t += G) scatter_phase(R, nb, pass, mn, t, ws);
+    grid_barrier(ws.ctl, G, k);
   }
-}
-
-// Present values per scan block.
-__global__ __launch_bounds__(kDenseBlk) void dense_blocksum_kernel(RadixWs ws) {
-  __shared__ uint32_t wsum[kDenseBlk / 64 + 1];
-  const uint64_t nv = ws.range[2];
-  if (!nv || (uint64_t)blockIdx.x * kDenseBlk >= nv) return;
-  const int32_t *count = dense_count(ws, nv);
-  const uint64_t v = (uint64_t)blockIdx.x * kDenseBlk + threadIdx.x;
-  const uint32_t pr = v < nv && count[v] > 0 ? 1u : 0u;
-  uint32_t total;
-  block_inclusive_scan<kDenseBlk>(pr, wsum, total);
-  if (threadIdx.x == 0) ws.hist[blockIdx.x] = total;
-}
-
-// Group numbers of the present values (ascending), and the per-group outputs.
-__global__ __launch_bounds__(kDenseBlk) void dense_groups_kernel(
-    RadixWs ws, int64_t *__restrict__ uk, int32_t *__restrict__ fi, int32_t *__restrict__ cnt,
-    int64_t *__restrict__ nu_out) {
-  __shared__ uint32_t wsum[kDenseBlk / 64 + 1];
-  const uint64_t nv = ws.range[2];
-  if (!nv || (uint64_t)blockIdx.x * kDenseBlk >= nv) return;
-  const uint64_t mn = ws.range[0];
-  const int32_t *first = dense_first(ws), *count = dense_count(ws, nv);
-  int32_t *gid = ws.idxB;
-  const int b = blockIdx.x, tid = threadIdx.x;
-  uint32_t before = 0;   // present values in all earlier blocks
-  for (int bb = tid; bb < b; bb += kDenseBlk) before += ws.hist[bb];
-  uint32_t g0;
-  block_inclusive_scan<kDenseBlk>(before, wsum, g0);
-  const uint64_t v = (uint64_t)b * kDenseBlk + tid;
-  const uint32_t pr = v < nv && count[v] > 0 ? 1u : 0u;
-  uint32_t total;
-  const uint32_t incl = block_inclusive_scan<kDenseBlk>(pr, wsum, total);
-  if (pr) {
-    const uint32_t g = g0 + incl - 1u;
-    uk[g] = unmap_key(mn + v);
-    fi[g] = first[v];
-    if (cnt) cnt[g] = count[v];
-    gid[v] = (int32_t)g;
+  for (int t = b; t < nb; t += G) heads_phase(R, npass, t, ws);
+  grid_barrier(ws.ctl, G, k);
+  if (b == 0) block_scan_inplace(ws.bheads, nb);
+  grid_barrier(ws.ctl, G, k);
+  for (int t = b; t < nb; t += G) compact_phase(R, npass, t, ws, uk, fi, inv, nu_out);
+  if (cnt) {
+    grid_barrier(ws.ctl, G, k);
+    const int64_t n = *nu_out;
+    for (int64_t g = (int64_t)b * kRadixThreads + threadIdx.x; g < R && g < n;
+         g += (int64_t)G * kRadixThreads)
+      cnt[g] = ws.start[g + 1] - ws.start[g];
   }
-  if ((uint64_t)(b + 1) * kDenseBlk >= nv && tid == 0) *nu_out = (int64_t)(g0 + total);
-}
-
-__global__ void dense_inverse_kernel(int R, RadixWs ws, int32_t *__restrict__ inv) {
-  const uint64_t nv = ws.range[2];
-  if (!nv) return;
-  const uint64_t mn = ws.range[0];
-  for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < R;
-       p += (int64_t)gridDim.x * blockDim.x)
-    inv[p] = ws.idxB[ws.keyA[p] - mn];
 }
 
 // ---------------------------------------------------------------- host side
@@ -633,15 +856,38 @@ static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t dedup_workspace_bytes(int64_t R) {
   if (R <= kSmallMax) return 0;
   size_t nb = (size_t)((R + kTile - 1) / kTile);
+  size_t nvb = (size_t)((R + kDenseBlk - 1) / kDenseBlk);
   size_t s = 0;
   s += 2 * align_up(sizeof(uint64_t) * R);
   s += 2 * align_up(sizeof(int32_t) * R);
-  s += 2 * align_up(sizeof(uint64_t) * nb);
+  s += 2 * align_up(sizeof(uint64_t) * kPrepMax);
   s += align_up(sizeof(uint64_t) * 4);
   s += align_up(sizeof(uint32_t) * kBins * nb);
+  s += align_up(sizeof(uint32_t) * kBins);
   s += align_up(sizeof(uint32_t) * nb);
   s += align_up(sizeof(int32_t) * (R + 1));
+  s += align_up(sizeof(uint64_t) * nvb);
+  s += align_up(sizeof(uint32_t) * kCtlWords);
   return s;
+}
+
+// Workgroups of radix_sort_kernel that the current device holds at once (0:
+// unknown).
+static int radix_capacity() {
+  static int cache[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cache[dev]) return cache[dev] > 0 ? cache[dev] : 0;
+  int cus = 0, per = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, radix_sort_kernel, kRadixThreads, 0) !=
+          hipSuccess ||
+      cus <= 0 || per <= 0) {
+    cache[dev] = -1;
+    return 0;
+  }
+  cache[dev] = cus * per;
+  return cache[dev];
 }
 
 hipError_t launch_dedup(const int64_t *keys, int64_t R, int64_t *uk, int32_t *fi, int32_t *cnt,
@@ -659,45 +905,47 @@ hipError_t launch_dedup(const int64_t *keys, int64_t R, int64_t *uk, int32_t *fi
                        P, uk, fi, cnt, inv, nu);
     return hipGetLastError();
   }
+  const int capacity = radix_capacity();
+  if (capacity <= 0) return hipErrorNotSupported;
   const int nb = (int)((R + kTile - 1) / kTile);
+  const int64_t nvb = (R + kDenseBlk - 1) / kDenseBlk;
   char *p = (char *)ws;
   RadixWs w;
   w.keyA = (uint64_t *)p; p += align_up(sizeof(uint64_t) * R);
   w.keyB = (uint64_t *)p; p += align_up(sizeof(uint64_t) * R);
   w.idxA = (int32_t *)p; p += align_up(sizeof(int32_t) * R);
   w.idxB = (int32_t *)p; p += align_up(sizeof(int32_t) * R);
-  w.pmin = (uint64_t *)p; p += align_up(sizeof(uint64_t) * nb);
-  w.pmax = (uint64_t *)p; p += align_up(sizeof(uint64_t) * nb);
+  w.pmin = (uint64_t *)p; p += align_up(sizeof(uint64_t) * kPrepMax);
+  w.pmax = (uint64_t *)p; p += align_up(sizeof(uint64_t) * kPrepMax);
   w.range = (uint64_t *)p; p += align_up(sizeof(uint64_t) * 4);
   w.hist = (uint32_t *)p; p += align_up(sizeof(uint32_t) * kBins * nb);
+  w.dtot = (uint32_t *)p; p += align_up(sizeof(uint32_t) * kBins);
   w.bheads = (uint32_t *)p; p += align_up(sizeof(uint32_t) * nb);
-  w.start = (int32_t *)p;
-  hipLaunchKernelGGL(radix_prep_kernel, dim3(nb), dim3(kRadixThreads), 0, st, keys, (int)R, w);
-  hipLaunchKernelGGL(radix_range_kernel, dim3(1), dim3(1024), 0, st, (int)R, nb, w);
-  // dense path (each kernel returns at once when the keys need the sort)
-  {
-    const unsigned vb = (unsigned)((R + kDenseBlk - 1) / kDenseBlk);   // nv <= R
-    hipLaunchKernelGGL(dense_clear_kernel, dim3(vb), dim3(kDenseBlk), 0, st, w);
-    hipLaunchKernelGGL(dense_mark_kernel, dim3((unsigned)((R + kAggRound - 1) / kAggRound)),
-                       dim3(256), 0, st, (int)R, w);
-    hipLaunchKernelGGL(dense_blocksum_kernel, dim3(vb), dim3(kDenseBlk), 0, st, w);
-    hipLaunchKernelGGL(dense_groups_kernel, dim3(vb), dim3(kDenseBlk), 0, st, w, uk, fi, cnt, nu);
-    hipLaunchKernelGGL(dense_inverse_kernel, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, st,
-                       (int)R, w, inv);
-  }
-  for (int pass = 0; pass < 64 / kRadixBits; ++pass) {
-    hipLaunchKernelGGL(radix_hist_kernel, dim3(nb), dim3(kRadixThreads), 0, st, (int)R, nb,
-                       pass, w);
-    hipLaunchKernelGGL(radix_scatter_kernel, dim3(nb), dim3(kRadixThreads), 0, st, (int)R, nb,
-                       pass, w);
-  }
-  hipLaunchKernelGGL(radix_heads_kernel, dim3(nb), dim3(kRadixThreads), 0, st, (int)R, w);
-  hipLaunchKernelGGL(radix_compact_kernel, dim3(nb), dim3(kRadixThreads), 0, st, (int)R, w, uk,
-                     fi, inv, nu);
-  if (cnt) {
-    hipLaunchKernelGGL(radix_counts_kernel, dim3((unsigned)((R + 255) / 256)), dim3(256), 0, st,
-                       (int)R, w, (const int64_t *)nu, cnt);
-  }
+  w.start = (int32_t *)p; p += align_up(sizeof(int32_t) * (R + 1));
+  w.flags = (uint64_t *)p; p += align_up(sizeof(uint64_t) * nvb);
+  w.ctl = (uint32_t *)p;
+  int Ri = (int)R;
+  const int64_t chunks = (R + kPrepChunk - 1) / kPrepChunk;
+  const int P = chunks < kPrepMax ? (int)chunks : kPrepMax;
+  hipLaunchKernelGGL(dedup_prep_kernel, dim3(P), dim3(kRadixThreads), 0, st, keys, Ri, w);
+  int64_t rounds = (R + kAggRound - 1) / kAggRound;
+  if (rounds > 4096) rounds = 4096;
+  hipLaunchKernelGGL(dense_mark_kernel, dim3((unsigned)rounds), dim3(kRadixThreads), 0, st, Ri,
+                     P, w);
+  hipLaunchKernelGGL(dense_groups_kernel, dim3((unsigned)nvb), dim3(kRadixThreads), 0, st, Ri,
+                     w, uk, fi, cnt, nu);
+  int64_t ib = (R + 255) / 256;
+  if (ib > 8192) ib = 8192;
+  hipLaunchKernelGGL(dense_inverse_kernel, dim3((unsigned)ib), dim3(256), 0, st, Ri, w, inv);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  int G = nb < kRadixGridMax ? nb : kRadixGridMax;
+  if (G > capacity) G = capacity;
+  // an ordinary launch: G is at most what the device holds at once, so every
+  // workgroup becomes resident (a cooperative launch would only add ~17 us of
+  // set-up to every call, the dense path's included)
+  hipLaunchKernelGGL(radix_sort_kernel, dim3(G), dim3(kRadixThreads), 0, st, Ri, nb, w, uk, fi,
+                     cnt, inv, nu);
   return hipGetLastError();
 }
 

@@ -124,3 +124,20 @@ def test_dedup_deterministic():
     b = _gpu_dedup(w.keys)
     np.testing.assert_array_equal(a[0], b[0])
     np.testing.assert_array_equal(a[1], b[1])
+
+
+@pytest.mark.parametrize("case", ["dense", "radix"])
+def test_dedup_more_tiles_than_workgroups(case):
+    # over 8M keys: 2,052 tiles of 4,096 keys, more than the prep launch
+    # (1,024) and the persistent sort (at most 256) have workgroups, so each
+    # takes several tiles; 8,193 value blocks in the dense scan's look-back
+    # chain; direct addressing (keys over a span below R) and the radix sort
+    rng = np.random.default_rng(5 if case == "dense" else 6)
+    R = (1 << 23) + 12_345
+    if case == "dense":
+        keys = rng.integers(-(1 << 22), 1 << 22, size=R).astype(np.int64)
+    else:
+        keys = rng.integers(0, 1 << 40, size=R).astype(np.int64)
+        keys[rng.random(R) < 0.3] = 17   # a hot key
+    note(f"dedup {case} R={R}")
+    _gpu_dedup(keys)
