@@ -121,6 +121,9 @@ def parse():
                     help="micro-batching (Eq. 8): score latency against batch size, and the "
                          "window's distinct queries scored in sub-batches of at most B or split "
                          "over k streams (mean / max completion); one JSON line of its own")
+    ap.add_argument("--batch-sizes", type=str, default=None,
+                    help="with --batch-curve: comma-separated batch sizes of the latency curve "
+                         "(default 1,2,4,...,2048)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
     return ap.parse_args()
@@ -616,7 +619,9 @@ def batch_curve_bench(args):
     m.q_unique[:R].copy_(q_req)
     torch.cuda.synchronize(dev)
     curve = []
-    for b in [1, 2, 4, 8, 16, 32, 64, 96, 128, 160, 256, 384, 512, 1024, 2048]:
+    sizes = ([int(x) for x in args.batch_sizes.split(",") if x.strip()] if args.batch_sizes
+             else [1, 2, 4, 8, 16, 32, 64, 96, 128, 160, 256, 384, 512, 1024, 2048])
+    for b in sizes:
         if b > R:
             break
         ms = timed(lambda: hs.hs_score_topk(m.plan, m.q_unique, b, None, corpus, scale,
