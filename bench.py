@@ -122,8 +122,9 @@ def parse():
                          "window's distinct queries scored in sub-batches of at most B or split "
                          "over k streams (mean / max completion); one JSON line of its own")
     ap.add_argument("--batch-sizes", type=str, default=None,
-                    help="with --batch-curve: comma-separated batch sizes of the latency curve "
-                         "(default 1,2,4,...,2048)")
+                    help="with --batch-curve: only the latency curve, at these comma-separated "
+                         "batch sizes (default: the full curve 1,2,4,...,2048 and the sub-batch "
+                         "and stream-split runs)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
     return ap.parse_args()
@@ -627,6 +628,18 @@ def batch_curve_bench(args):
         ms = timed(lambda: hs.hs_score_topk(m.plan, m.q_unique, b, None, corpus, scale,
                                             m.topk_score, m.topk_index, m.ws, stream=stream))
         curve.append({"batch": b, "ms": round(ms, 4), "queries_per_s": round(b / ms * 1e3, 1)})
+
+    if args.batch_sizes:   # the latency curve alone
+        worst = max(curve, key=lambda c: c["ms"])
+        out = {"metric": "score latency vs batch size (Eq. 8, Appendix A batch limit)",
+               "value": round(worst["batch"] / worst["ms"] * 1e3, 1), "unit": "queries/s",
+               "n_gpus": 1, "steps": reps, "warmup": 2, "ms_per_step": worst["ms"],
+               "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+               "dtype": "bf16", "data": "synthetic",
+               "config": {"workload": f"{cfg.name}: {cfg.desc}", "k": k, "n_corpus": N},
+               "latency_curve": curve}
+        print(json.dumps(out), flush=True)
+        return
 
     # the window's distinct queries in sub-batches of at most B, one after another
     m.gather_queries(q_req, stream)
