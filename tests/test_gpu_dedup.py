@@ -141,3 +141,29 @@ def test_dedup_more_tiles_than_workgroups(case):
         keys[rng.random(R) < 0.3] = 17   # a hot key
     note(f"dedup {case} R={R}")
     _gpu_dedup(keys)
+
+
+@pytest.mark.parametrize("tiles", [64, 65, 257])
+def test_radix_digit_offsets_around_the_tile_threshold(tiles):
+    # the sort takes its digit offsets straight from the histogram up to 64
+    # tiles of 4,096 keys and from per-digit row scans above; 257 tiles is
+    # more than the persistent sort's 256 workgroups (one takes two tiles);
+    # ragged last tile, hot keys, negative keys
+    rng = np.random.default_rng(100 + tiles)
+    R = tiles * 4096 - 1000
+    keys = rng.integers(-(1 << 62), 1 << 62, size=R).astype(np.int64)
+    keys[rng.random(R) < 0.2] = -5
+    keys[rng.random(R) < 0.1] = 1 << 61
+    note(f"dedup radix R={R} ({tiles} tiles)")
+    _gpu_dedup(keys)
+
+
+def test_dense_and_sort_paths_alternate_on_one_workspace():
+    # the same plan and workspace for a dense-range batch, then a sort-path
+    # batch, then dense again: every launch resets the scratch it needs
+    rng = np.random.default_rng(77)
+    R = 40_000
+    dense = rng.integers(0, R // 2, size=R).astype(np.int64)
+    wide = rng.integers(-(1 << 40), 1 << 40, size=R).astype(np.int64)
+    for k in (dense, wide, dense, wide):
+        _gpu_dedup(k)
