@@ -3,9 +3,9 @@
 // HeraSys Sec. 3.3 (I): a node whose signature matches a node already in the
 // window is fused into it; Eq. (3) aggregates over the merged set M(v*).  The
 // paper detects matches with a hash map (Appendix B.3, Phase 1).  On the GPU
-// the same groups come out of a stable sort of (key, request) pairs, which
-// also makes every output canonical: distinct keys ascending, the survivor of
-// a group is its earliest request, counts[g] = |M(v*)|, inverse[i] = group.
+// every path below gives the same canonical outputs (those of a stable sort
+// of (key, request) pairs): distinct keys ascending, the survivor of a group
+// is its earliest request, counts[g] = |M(v*)|, inverse[i] = group.
 //
 // Three paths:
 //   R <= kHashMax  : one workgroup groups the keys in an LDS hash table
