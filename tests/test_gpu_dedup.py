@@ -167,3 +167,54 @@ def test_dense_and_sort_paths_alternate_on_one_workspace():
     wide = rng.integers(-(1 << 40), 1 << 40, size=R).astype(np.int64)
     for k in (dense, wide, dense, wide):
         _gpu_dedup(k)
+
+
+def test_sort_path_beside_a_concurrent_score_call():
+    # the sort runs as one persistent launch whose workgroups wait for each
+    # other at grid barriers; a score call on a second stream (a persistent
+    # grid of its own, one workgroup on every CU) runs at the same time: both
+    # finish and both are exact
+    import oracle
+    import paper_2607_22578_amd as hs
+    from gpu_harness import check_dedup, check_unique_topk, to_dev
+    dev = device()
+    w = synth.make("ridge1m", n_corpus=1, with_corpus=False)
+    N = 400_000   # a score call of ~0.3 ms, longer than the sort
+    c, _ = synth.gaussian_rows(w.seed, synth.S_CORPUS, N, w.dim, "bf16")
+    m = hs.MergedRetrieval(w.R, w.dim, N, w.k, hs.HS_BF16, hs.HS_BF16, device=dev)
+    st = torch.cuda.current_stream(dev)
+    cd = to_dev(c)
+    nu = m.dedup(to_dev(w.keys), st, host_count=True)
+    m.gather_queries(to_dev(w.q_req), st)
+    torch.cuda.synchronize(dev)
+    ref_w = check_dedup(m, w.keys)
+
+    rng = np.random.default_rng(31)
+    R = 300_000
+    keys = rng.integers(-(1 << 50), 1 << 50, size=R).astype(np.int64)
+    keys[rng.random(R) < 0.25] = 12345
+    ref = oracle.dedup(keys)
+    plan = hs.hs_merge_plan(R, 8, 1, 1, hs.HS_BF16, hs.HS_BF16)
+    ws = torch.empty(max(plan.workspace_bytes, 256), dtype=torch.uint8, device=dev)
+    kdev = torch.from_numpy(keys).to(dev)
+    uk = torch.empty(R, dtype=torch.int64, device=dev)
+    fi = torch.empty(R, dtype=torch.int32, device=dev)
+    ct = torch.empty(R, dtype=torch.int32, device=dev)
+    inv = torch.empty(R, dtype=torch.int32, device=dev)
+    n_dev = torch.empty(1, dtype=torch.int64, device=dev)
+    other = torch.cuda.Stream(dev)   # default priority
+    for rep in range(3):
+        note(f"concurrent sort + score, repetition {rep}")
+        m.topk_score.zero_()
+        m.topk_index.zero_()
+        torch.cuda.synchronize(dev)
+        m.score_chunked(cd, nu, nu, None, other)
+        hs.hs_dedup(plan, kdev, uk, fi, ct, inv, n_dev, None, ws, stream=st)
+        torch.cuda.synchronize(dev)
+        n = int(n_dev.item())
+        assert n == ref["n_unique"]
+        np.testing.assert_array_equal(uk[:n].cpu().numpy(), ref["unique_keys"])
+        np.testing.assert_array_equal(fi[:n].cpu().numpy(), ref["first_index"])
+        np.testing.assert_array_equal(ct[:n].cpu().numpy(), ref["counts"])
+        np.testing.assert_array_equal(inv.cpu().numpy(), ref["inverse"])
+        check_unique_topk(m, ref_w, w.q_req, c, w.k, sel=np.array([0, nu // 2, nu - 1]))
