@@ -516,3 +516,59 @@ class MergedRetrieval:
                           stream=streams[j])
             base += nb
 
+
+
+# ---------------------------------------------------------------- one call
+
+def dedup(keys, stream=None):
+    """Step 1 alone (Sec. 3.3 (I) signature matching) on a device int64
+    tensor of R keys: returns (unique_keys, first_index, counts, inverse),
+    the per-group tensors trimmed to the n_u groups.  Reads n_u on the host
+    (one synchronisation of `stream`)."""
+    import torch
+    if keys.dtype != torch.int64 or keys.dim() != 1:
+        raise TypeError("keys must be a 1-D int64 tensor")
+    R = keys.shape[0]
+    dev = keys.device
+    stream = stream if stream is not None else torch.cuda.current_stream(dev)
+    plan = hs_merge_plan(R, 8, 1, 1, HS_BF16, HS_BF16)
+    R1 = max(R, 1)
+    ws = torch.empty(max(plan.workspace_bytes, 256), dtype=torch.uint8, device=dev)
+    uk = torch.empty(R1, dtype=torch.int64, device=dev)
+    fi = torch.empty(R1, dtype=torch.int32, device=dev)
+    ct = torch.empty(R1, dtype=torch.int32, device=dev)
+    inv = torch.empty(R1, dtype=torch.int32, device=dev)
+    nu_dev = torch.zeros(1, dtype=torch.int64, device=dev)
+    nu = hs_dedup(plan, keys if R else None, uk, fi, ct, inv, nu_dev, True, ws, stream=stream)
+    return uk[:nu], fi[:nu], ct[:nu], inv[:R]
+
+
+def merge_retrieval(keys, q_req, corpus, k: int, scale=None, workflow_offsets=None,
+                    max_unique: int = 0, stream=None):
+    """The whole window in one call: dedup (Sec. 3.3 (I)), one batched exact
+    top-k retrieval per distinct query (Appendix A batching), delivery of each
+    group's result to every request (Sec. 3.3 (I)).  keys [R] int64,
+    q_req [R x d] (float32 or bfloat16), corpus [N x d] (float32, bfloat16, or
+    float8_e4m3fn / uint8 codes with scale [N] float32), all on one device;
+    workflow_offsets: host CSR of W + 1 request offsets, or None for one
+    workflow.  Returns a dict of device tensors: out_score / out_index
+    [R x k] (per request), unique_keys / first_index / counts [n_u],
+    inverse [R], topk_score / topk_index [n_u x k], and n_unique (an int:
+    the call reads it on the host once) and `retrieval`, the MergedRetrieval
+    that owns them (workflow_results(w) gives workflow w's rows)."""
+    import torch
+    stream = stream if stream is not None else torch.cuda.current_stream(keys.device)
+    R, d = q_req.shape
+    N = corpus.shape[0]
+    offs = None if workflow_offsets is None else [int(x) for x in workflow_offsets]
+    W = 1 if offs is None else len(offs) - 1
+    m = MergedRetrieval(R, d, N, k, dtype_code(q_req), dtype_code(corpus), device=keys.device,
+                        max_unique=max_unique, n_workflows=W, workflow_offsets=offs)
+    m.run(keys, q_req, corpus, scale, stream=stream)
+    stream.synchronize()
+    nu = int(m.n_unique.item())
+    return {"out_score": m.out_score[:R], "out_index": m.out_index[:R],
+            "unique_keys": m.unique_keys[:nu], "first_index": m.first_index[:nu],
+            "counts": m.counts[:nu], "inverse": m.inverse[:R],
+            "topk_score": m.topk_score[:nu], "topk_index": m.topk_index[:nu],
+            "n_unique": nu, "retrieval": m}
