@@ -374,6 +374,8 @@ def main():
         tr = json.load(open(tf))
         if tr.get("kernel_source") == src_hash:
             roof["traffic"] = tr.get("hbm_bytes_per_launch")
+            # bytes beyond L2 (counters) per second of the timed score step
+            roof["traffic_gbs"] = round(roof["traffic"] / t_s / 1e9, 1)
 
     value = R * args.steps / (total_ms * 1e-3)
     out = {
@@ -570,6 +572,7 @@ def dedup_bench(args):
         tr = json.load(open(DEDUP_TRAFFIC_FILE))
         if tr.get("kernel_source") == out["roofline"]["kernel_source"]:
             out["roofline"]["traffic"] = tr.get("hbm_bytes_per_step")
+            out["roofline"]["traffic_gbs"] = round(out["roofline"]["traffic"] / t / 1e9, 1)
     print(json.dumps(out), flush=True)
 
 
