@@ -74,6 +74,23 @@ constexpr int kMKC = 64;                 // K per ring stage (four 16-deep MFMA 
 constexpr int kMQcap = 8;                // queue slots per query and round
 constexpr int kMVals = 16 * kMRB;        // scores per lane and query per tile
 constexpr int kMLanesQ = kMW * 2;        // lanes holding one query in a tile
+
+// Seed pass sample: the lane maxima of the first T tiles of every slice (at
+// most kSeedMax of them per query).  T is one for k <= 48.  For larger k the
+// k-th largest lane maximum of one tile per slice is a weak bound (k is then a
+// sizeable fraction of the sample) and every row that passes it costs a list
+// insertion, so T grows to 16 as long as the sample stays within 1/64 of the
+// slice's tiles and within kSeedMax values.
+constexpr int kSeedMax = 8192;
+constexpr int kSeedTilesMax = 16;
+__host__ __device__ __forceinline__ int seed_tiles(int k, int64_t ntiles, int64_t S) {
+  if (k <= 48 || S < 1) return 1;
+  int64_t t = ntiles / (S * 64);
+  const int64_t room = kSeedMax / (S * kMLanesQ);
+  if (t > room) t = room;
+  if (t > kSeedTilesMax) t = kSeedTilesMax;
+  return t < 1 ? 1 : (int)t;
+}
 constexpr int kMSplitMaxSK = 8192;       // bound on S*k (merge list length)
 constexpr int kMRowsW = 32 * kMRB;       // rows per wave in a tile
 constexpr int kMSS = kMNC + 128 - kMRowsW;  // row-scale slot stride (floats): the
@@ -233,7 +250,7 @@ struct MfmaArgs {
   int grid;
   uint64_t *part;
   uint32_t *gthr;   // [cap] per-query shared thresholds (ordered score, 0 = none)
-  uint32_t *lmax;   // [n_u][S][8] lane maxima of the seed pass (ordered scores)
+  uint32_t *lmax;   // [n_u][S][T][8] lane maxima of the seed pass (ordered scores)
 };
 
 // Fragments of one half stage (two 16-deep steps).  The K order inside a
@@ -387,6 +404,7 @@ __device__ __forceinline__ MLds carve_mlds(unsigned char *p, int k) {
 struct MItem {
   int qbase, qvalid, s;
   int64_t S;
+  int T;   // tiles per slice of the seed pass sample
 };
 
 // Publish query t's threshold (a lower bound of its k-th best score over its
@@ -602,14 +620,15 @@ __device__ __forceinline__ void warm_minima(const MLds &L, f32x16m (&acc)[kMRB][
 }
 
 // Seed pass: each lane's best score of the tile for each of its queries, as
-// an ordered score, to lmax[(query * S + slice) * 8 + lane-of-query].  These
+// an ordered score, to lmax[((query * S + slice) * T + t) * 8 + lane-of-query]
+// for the slice's t-th sampled tile (T tiles per slice).  These
 // are scores of distinct corpus rows, so the k-th largest of all of a
 // query's lane maxima (over all slices) is a lower bound of its k-th best
 // score over the whole corpus.
 template <bool FP8, int NQB>
 __device__ __forceinline__ void mtile_lane_maxima(const MfmaArgs &a, const MItem &it,
                                                   f32x16m (&acc)[kMRB][NQB], int row0,
-                                                  const float *ssc) {
+                                                  const float *ssc, int t) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int c = lane & 31, h = lane >> 5;
   const int lrow = wv * 32 * kMRB + 4 * h;
@@ -626,7 +645,7 @@ __device__ __forceinline__ void mtile_lane_maxima(const MfmaArgs &a, const MItem
       for (int i = 0; i < 16; ++i) m = fmaxf(m, acc[rb][qb][i]);
     const int ql = qb * 32 + c;
     if (ql < it.qvalid)
-      a.lmax[((int64_t)(it.qbase + ql) * it.S + it.s) * kMLanesQ + wv * 2 + h] =
+      a.lmax[(((int64_t)(it.qbase + ql) * it.S + it.s) * it.T + t) * kMLanesQ + wv * 2 + h] =
           m > -__builtin_inff() ? ord_score(m) : 0u;
   }
 }
@@ -812,10 +831,11 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
     const int qt = w % (int)sp.qtiles;
     it.s = w / (int)sp.qtiles;
     it.S = sp.S;
+    it.T = seed_tiles(a.k, sp.ntiles, sp.S);
     const int s0 = (int)((int64_t)it.s * sp.ntiles / sp.S);
     const int s1 = (int)((int64_t)(it.s + 1) * sp.ntiles / sp.S);
     const int t0 = s0;
-    const int t1 = SEED && s1 > s0 ? s0 + 1 : s1;
+    const int t1 = SEED ? s0 + (s1 - s0 < it.T ? s1 - s0 : it.T) : s1;
     it.qbase = qt * kMMQ;
     it.qvalid = (int)(nu - it.qbase < kMMQ ? nu - it.qbase : kMMQ);
     const int ntl = t1 - t0;
@@ -1030,7 +1050,7 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
       for (int j = 1; j < nch; ++j) stage(std::false_type{}, j + 1 < nch);
       if constexpr (SEED)
         mtile_lane_maxima<FP8>(a, it, acc, (t0 + tl) * kMNC,
-                               FP8 ? L.sscale + e_sc * kMSS : nullptr);
+                               FP8 ? L.sscale + e_sc * kMSS : nullptr, tl);
       else
         mtile_epilogue<FP8, LDS_LISTS>(L, a, it, acc, thr_r, epoch, (t0 + tl) * kMNC,
                                        FP8 ? L.sscale + e_sc * kMSS : nullptr,
@@ -1040,6 +1060,13 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
       read_frags<FP8>(f0, L.ring + r_slot * G::stage, wv, c, h, 0);
     }
 
+    if constexpr (SEED) {   // sampled tiles this slice does not have: no value
+      const int st = it.T;
+      for (int e = tid; e < it.qvalid * (st - ntl) * kMLanesQ; e += kMT) {
+        const int q = e / ((st - ntl) * kMLanesQ), r = e % ((st - ntl) * kMLanesQ);
+        a.lmax[(((int64_t)(it.qbase + q) * it.S + it.s) * st + ntl) * kMLanesQ + r] = 0u;
+      }
+    }
     // merge what is still queued, then flush the LDS lists of this item
     if constexpr (!SEED) {
       bar_lds();
@@ -1102,8 +1129,10 @@ int persistent_grid(bool mfma);
 // (rounded to 256 bytes) followed by the partial lists.
 size_t mfma_thr_bytes(int64_t cap) { return ((size_t)cap * 4 + 255) & ~(size_t)255; }
 
-// worst case over n_u in [1, cap] and grids up to grid_max of n_u * S * f(k)
-static size_t mfma_split_worst(int64_t cap, int64_t N, int k, int grid_max, size_t per_slice) {
+// worst case over n_u in [1, cap] and grids up to grid_max of n_u * S * f(k),
+// f(k) = per_slice bytes, times the seed pass's tiles per slice if seed
+static size_t mfma_split_worst(int64_t cap, int64_t N, int k, int grid_max, size_t per_slice,
+                               bool seed = false) {
   size_t best = 0;
   const int64_t qtmax = (cap + kMMQ - 1) / kMMQ;
   int64_t smax = kMSplitMaxSK / k;
@@ -1112,7 +1141,8 @@ static size_t mfma_split_worst(int64_t cap, int64_t N, int k, int grid_max, size
     const int64_t nu = qt * kMMQ < cap ? qt * kMMQ : cap;
     for (int64_t g = 8; g <= grid_max; g += 8) {
       const Split sp = make_split(nu, N, kMMQ, kMNC, g, smax);
-      const size_t b = (size_t)nu * (size_t)sp.S * per_slice;
+      const size_t b = (size_t)nu * (size_t)sp.S * per_slice *
+                       (seed ? (size_t)seed_tiles(k, sp.ntiles, sp.S) : 1u);
       if (b > best) best = b;
     }
   }
@@ -1120,10 +1150,10 @@ static size_t mfma_split_worst(int64_t cap, int64_t N, int k, int grid_max, size
 }
 
 // Score workspace of the matrix-core path: [shared thresholds, cap x u32 |
-// seed-pass lane maxima, n_u x S x 8 u32 | partial lists, n_u x S x k keys],
+// seed-pass lane maxima, n_u x S x T x 8 u32 | partial lists, n_u x S x k keys],
 // each rounded to 256 bytes.
 size_t mfma_lmax_bytes(int64_t cap, int64_t N, int k, int grid_max) {
-  return mfma_split_worst(cap, N, k, grid_max, (size_t)kMLanesQ * 4);
+  return mfma_split_worst(cap, N, k, grid_max, (size_t)kMLanesQ * 4, true);
 }
 
 size_t mfma_partial_bytes(int64_t cap, int64_t N, int k, int grid_max) {
@@ -1161,7 +1191,6 @@ static hipError_t launch_mfma(K kern, int grid, int lds, const MfmaArgs &a, hipS
 // values that carry the digits chosen so far by their next digit, and keeps
 // the largest digit whose count of values at or above it reaches the rank
 // still sought.
-constexpr int kSeedMax = 8192;
 constexpr int kSeedThreads = 256;
 __global__ __launch_bounds__(kSeedThreads) void mfma_seed_kernel(
     const uint32_t *__restrict__ lmax, int64_t n_unique, const int64_t *__restrict__ nu_dev,
@@ -1171,7 +1200,7 @@ __global__ __launch_bounds__(kSeedThreads) void mfma_seed_kernel(
   __shared__ uint32_t sel[2];   // chosen digit, values above it
   const int64_t nu = read_nu(n_unique, nu_dev, cap);
   const Split sp = make_split(nu, N, kMMQ, kMNC, grid, smax);
-  const int64_t per = sp.S * kMLanesQ;
+  const int64_t per = sp.S * kMLanesQ * seed_tiles(k, sp.ntiles, sp.S);
   const int n = (int)(per < kSeedMax ? per : kSeedMax);
   const int tid = threadIdx.x;
   if (n < k) {   // fewer lane maxima than k: no seed

@@ -2,8 +2,9 @@
 the oracle (acceptance rule of oracle/accept.py): dimensions that leave a
 partial last K stage (the copies read zeros past d), corpora smaller than
 one 384-row tile or with a ragged last tile, k-lists held in global memory
-instead of LDS, k too large for the first-pass threshold seed, and a merge
-with more survivors than it ranks by counting (it sorts them)."""
+instead of LDS, k too large for the first-pass threshold seed, a seed that
+samples several tiles per slice (k > 48), and a merge with more survivors
+than it ranks by counting (it sorts them)."""
 import numpy as np
 import pytest
 
@@ -77,4 +78,24 @@ def test_large_k_many_survivors():
     ref = check_dedup(m, w.keys)
     sel = np.random.default_rng(7).choice(ref["n_unique"], size=48, replace=False)
     check_unique_topk(m, ref, q, c, k, sel=np.sort(sel))
+    check_delivery(m, w.R)
+
+
+@pytest.mark.parametrize("enc", ["bf16", "fp8"])
+def test_large_k_seed_samples_several_tiles(enc):
+    # k = 100 over the 20M-row workload's request stream (2,197 distinct
+    # queries: 18 query tiles, 14 slices on a 256-workgroup grid) and
+    # 1,200,000 rows (3,125 tiles, 223 per slice): for k > 48 the seed pass
+    # samples the first 223 / 64 = 3 tiles of every slice instead of one, so
+    # the seed and the shared thresholds come from 3 x 14 x 8 lane maxima
+    # per query
+    w = synth.make("fp8_20m", n_corpus=1, with_corpus=False)
+    d, n_corpus, k = 128, 1_200_000, 100
+    q, _ = synth.gaussian_rows(w.seed, synth.S_QUERY, 0, d, "bf16", row_ids=w.template_ids)
+    c, sc = synth.gaussian_rows(w.seed, synth.S_CORPUS, n_corpus, d, enc)
+    note(f"{enc} k={k} N={n_corpus} d={d}")
+    m = run_merge(w.keys, q, c, k, scale=sc if enc == "fp8" else None)
+    ref = check_dedup(m, w.keys)
+    sel = np.random.default_rng(11).choice(ref["n_unique"], size=40, replace=False)
+    check_unique_topk(m, ref, q, c, k, scale=sc if enc == "fp8" else None, sel=np.sort(sel))
     check_delivery(m, w.R)
