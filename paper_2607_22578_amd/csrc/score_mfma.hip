@@ -78,14 +78,16 @@ constexpr int kMLanesQ = kMW * 2;        // lanes holding one query in a tile
 // Seed pass sample: the lane maxima of the first T tiles of every slice (at
 // most kSeedMax of them per query).  T is one for k <= 48.  For larger k the
 // k-th largest lane maximum of one tile per slice is a weak bound (k is then a
-// sizeable fraction of the sample) and every row that passes it costs a list
-// insertion, so T grows to 16 as long as the sample stays within 1/64 of the
-// slice's tiles and within kSeedMax values.
-constexpr int kSeedMax = 8192;
-constexpr int kSeedTilesMax = 16;
+// sizeable fraction of the sample): a sample of M rows lets about N k / M rows
+// of the corpus pass it, each a list insertion, and with many slices the
+// lists do not fill before their slice ends, so their own minima never take
+// over.  T therefore grows to 32 as long as the sample stays within 1/16 of
+// the slice's tiles and within kSeedMax values.
+constexpr int kSeedMax = 16384;
+constexpr int kSeedTilesMax = 32;
 __host__ __device__ __forceinline__ int seed_tiles(int k, int64_t ntiles, int64_t S) {
   if (k <= 48 || S < 1) return 1;
-  int64_t t = ntiles / (S * 64);
+  int64_t t = ntiles / (S * 16);
   const int64_t room = kSeedMax / (S * kMLanesQ);
   if (t > room) t = room;
   if (t > kSeedTilesMax) t = kSeedTilesMax;

@@ -86,8 +86,8 @@ def test_large_k_seed_samples_several_tiles(enc):
     # k = 100 over the 20M-row workload's request stream (2,197 distinct
     # queries: 18 query tiles, 14 slices on a 256-workgroup grid) and
     # 1,200,000 rows (3,125 tiles, 223 per slice): for k > 48 the seed pass
-    # samples the first 223 / 64 = 3 tiles of every slice instead of one, so
-    # the seed and the shared thresholds come from 3 x 14 x 8 lane maxima
+    # samples the first 223 / 16 = 13 tiles of every slice instead of one, so
+    # the seed and the shared thresholds come from 13 x 14 x 8 lane maxima
     # per query
     w = synth.make("fp8_20m", n_corpus=1, with_corpus=False)
     d, n_corpus, k = 128, 1_200_000, 100
