@@ -376,7 +376,7 @@ struct MLds {
   uint32_t *pub;     // [MQ] last threshold published to the shared array
   uint64_t *lmin;    // [MQ] last key of the sorted list when full, else its fill count
   float *warm;       // [kMW][MQ] per-wave minima of group maxima (aliases queue)
-  int32_t *flags;    // [1] overflow epoch, [2] half-full epoch
+  int32_t *flags;    // [1] overflow epoch, [2] merge-due epoch
   uint64_t *lists;   // [MQ][k] or nullptr (lists in the global partial buffer)
   uint64_t *tail;    // [MQ][kMTail] last entries of the global lists, or nullptr
 };
@@ -737,9 +737,13 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
   // Scores at or above the current threshold are appended to the per-query
   // LDS queues (atomics, no barrier).  Merges into the k-lists are deferred:
   // one barrier per tile checks whether some queue overflowed (its
-  // candidates stay eligible) or is half full; only then do the threads of
-  // the queries merge, the thresholds rise, and the candidates left over
-  // are examined again.
+  // candidates stay eligible) or is due for a merge; only then do the
+  // threads of the queries merge, the thresholds rise, and the candidates
+  // left over are examined again.  A queue is due when half full if the
+  // lists are in LDS, and only when full if they are in global memory,
+  // where a merge round (two barriers and climbs through global memory)
+  // costs more than the candidates a later threshold rise would save.
+  constexpr int qdue = LDS_LISTS ? kMQcap / 2 : kMQcap;
   for (;;) {
     bool ovf = false, full = false;
     pin_acc(acc);
@@ -788,7 +792,7 @@ __device__ __forceinline__ void mtile_epilogue(const MLds &L, const MfmaArgs &a,
           for (int i = 0; i < 4; ++i) w4[i] = (w8[2 * i] & ~m1) | (w8[2 * i + 1] & m1);
           const uint32_t w2a = (w4[0] & ~m2) | (w4[1] & m2), w2b = (w4[2] & ~m2) | (w4[3] & m2);
           const float sc = __uint_as_float((w2a & ~m3) | (w2b & m3));
-          full |= slot + 1 >= kMQcap / 2;
+          full |= slot + 1 >= qdue;
           L.queue[ql * kMQcap + slot] = make_key(sc, (uint32_t)(rowb + 8 * (jx >> 2) + (jx & 3)));
           ++slot;
         }
