@@ -131,6 +131,16 @@ __device__ __forceinline__ int swz_slot(int p, int row) {
 }
 
 constexpr int kMTail = 16;   // list entries kept in LDS when the lists are global
+
+// Order statistics a finished item publishes per query: level l holds the
+// ordered score of the ceil(k / r)-th best key of the slice's final list,
+// r = 2^l, l < kLvl (0 where the list is shorter).  If r slices publish level-l
+// values of at least x, those slices hold r * ceil(k / r) >= k distinct
+// rows scoring at least x, so the r-th largest level-l value over the
+// slices is a lower bound of the query's k-th best score.  An item starts
+// by raising the query's shared threshold to the best such bound over the
+// slices finished so far.
+constexpr int kLvl = 5;
 constexpr int kMWarmBytes = kMW * kMMQ * 4;   // per-wave warm-up minima (alias the queue)
 static_assert(kMWarmBytes <= kMMQ * kMQcap * 8, "warm-up minima fit in the queue");
 
@@ -253,6 +263,7 @@ struct MfmaArgs {
   uint64_t *part;
   uint32_t *gthr;   // [cap] per-query shared thresholds (ordered score, 0 = none)
   uint32_t *lmax;   // [n_u][S][T][8] lane maxima of the seed pass (ordered scores)
+  uint32_t *lvl;    // [n_u][kLvl][S] order statistics of finished items (ordered scores)
 };
 
 // Fragments of one half stage (two 16-deep steps).  The K order inside a
@@ -420,6 +431,51 @@ __device__ __forceinline__ void publish_thr(const MLds &L, const MfmaArgs &a, co
     L.pub[t] = o;
     atomicMax(a.gthr + it.qbase + t, o);
   }
+}
+
+// Keep t (descending) the R largest of the values offered so far.
+template <int R>
+__device__ __forceinline__ void offer_top(uint32_t (&t)[R], uint32_t x) {
+#pragma unroll
+  for (int u = 0; u < R; ++u) {
+    const uint32_t hi = t[u] > x ? t[u] : x;
+    x = t[u] > x ? x : t[u];
+    t[u] = hi;
+  }
+}
+
+// Best lower bound of a query's k-th best score from the order statistics
+// its finished slices published: the largest over levels l of the 2^l-th
+// largest level-l value over the S slices (0 if none).  lv = the query's
+// [kLvl][S] row; device-scope loads (other workgroups publish), issued 8
+// slices x kLvl levels at a time.
+__device__ __forceinline__ uint32_t level_bound(const uint32_t *lv, int S) {
+  static_assert(kLvl == 5, "one top buffer per level");
+  uint32_t t0[1] = {0u}, t1[2] = {0u, 0u}, t2[4] = {}, t3[8] = {}, t4[16] = {};
+  for (int s0 = 0; s0 < S; s0 += 8) {
+    uint32_t v[kLvl][8];
+#pragma unroll
+    for (int l = 0; l < kLvl; ++l)
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        v[l][u] = s0 + u < S ? __hip_atomic_load(lv + l * S + s0 + u, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT)
+                             : 0u;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      offer_top(t0, v[0][u]);
+      offer_top(t1, v[1][u]);
+      offer_top(t2, v[2][u]);
+      offer_top(t3, v[3][u]);
+      offer_top(t4, v[4][u]);
+    }
+  }
+  uint32_t b = t0[0];
+  b = t1[1] > b ? t1[1] : b;
+  b = t2[3] > b ? t2[3] : b;
+  b = t3[7] > b ? t3[7] : b;
+  b = t4[15] > b ? t4[15] : b;
+  return b;
 }
 
 // Merge the queued keys of query t into its k-list (one thread per query).
@@ -855,6 +911,15 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
       L.lmin[tid] = 0ull;
       L.pub[tid] = 0u;
       if (tid < it.qvalid && !SEED) {
+        // (items of the first round start before any item has finished)
+        if (w >= a.grid) {
+          const uint32_t b =
+              level_bound(a.lvl + (int64_t)(it.qbase + tid) * kLvl * it.S, (int)it.S);
+          if (b) {
+            atomicMax(a.gthr + it.qbase + tid, b);
+            L.pub[tid] = b;
+          }
+        }
         if (LDS_LISTS) {
           for (int j = 0; j < a.k; ++j) L.lists[tid * a.k + j] = 0ull;
         } else {
@@ -1076,7 +1141,28 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
     // merge what is still queued, then flush the LDS lists of this item
     if constexpr (!SEED) {
       bar_lds();
-      if (tid < it.qvalid) merge_queue<LDS_LISTS>(L, a, it, tid);
+      if (tid < it.qvalid) {
+        merge_queue<LDS_LISTS>(L, a, it, tid);
+        // this slice's order statistics for the items that start later
+        const uint64_t mn = L.lmin[tid];
+        const int fill = (mn >> 32) ? a.k : (int)mn;
+        const uint64_t *gl = a.part + ((int64_t)(it.qbase + tid) * it.S + it.s) * a.k;
+        uint32_t *lv = a.lvl + (int64_t)(it.qbase + tid) * kLvl * it.S + it.s;
+        for (int l = 0; l < kLvl; ++l) {
+          const int p = opaque(((a.k + (1 << l) - 1) >> l) - 1);   // ceil(k / 2^l) - 1
+          if (p < fill) {
+            uint64_t key;
+            if (LDS_LISTS)
+              key = L.lists[tid * a.k + p];
+            else if (p >= a.k - kMTail)
+              key = L.tail[tid * kMTail + p - (a.k - kMTail)];
+            else
+              key = gl[p];
+            __hip_atomic_store(lv + l * it.S, (uint32_t)(key >> 32), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+          }
+        }
+      }
     }
     if (LDS_LISTS && !SEED) {
       bar_lds();
@@ -1156,20 +1242,28 @@ static size_t mfma_split_worst(int64_t cap, int64_t N, int k, int grid_max, size
 }
 
 // Score workspace of the matrix-core path: [shared thresholds, cap x u32 |
-// seed-pass lane maxima, n_u x S x T x 8 u32 | partial lists, n_u x S x k keys],
+// seed-pass lane maxima, n_u x S x T x 8 u32 | order statistics of finished
+// items, n_u x kLvl x S u32 | partial lists, n_u x S x k keys],
 // each rounded to 256 bytes.
 size_t mfma_lmax_bytes(int64_t cap, int64_t N, int k, int grid_max) {
   return mfma_split_worst(cap, N, k, grid_max, (size_t)kMLanesQ * 4, true);
 }
 
+// published order statistics, n_u x S x kLvl u32
+static size_t mfma_lvl_bytes(int64_t cap, int64_t N, int k, int grid_max) {
+  return mfma_split_worst(cap, N, k, grid_max, (size_t)kLvl * 4);
+}
+
 size_t mfma_partial_bytes(int64_t cap, int64_t N, int k, int grid_max) {
   return mfma_thr_bytes(cap) + mfma_lmax_bytes(cap, N, k, grid_max) +
+         mfma_lvl_bytes(cap, N, k, grid_max) +
          mfma_split_worst(cap, N, k, grid_max, (size_t)k * 8);
 }
 
 // Offset of the partial lists in the score workspace.
 size_t mfma_part_offset(int64_t cap, int64_t N, int k, int grid_max) {
-  return mfma_thr_bytes(cap) + mfma_lmax_bytes(cap, N, k, grid_max);
+  return mfma_thr_bytes(cap) + mfma_lmax_bytes(cap, N, k, grid_max) +
+         mfma_lvl_bytes(cap, N, k, grid_max);
 }
 
 void mfma_split_params(int *mq, int *nc, int64_t *smax, int k) {
@@ -1200,7 +1294,8 @@ static hipError_t launch_mfma(K kern, int grid, int lds, const MfmaArgs &a, hipS
 constexpr int kSeedThreads = 256;
 __global__ __launch_bounds__(kSeedThreads) void mfma_seed_kernel(
     const uint32_t *__restrict__ lmax, int64_t n_unique, const int64_t *__restrict__ nu_dev,
-    int64_t cap, int64_t N, int k, int64_t smax, int grid, uint32_t *__restrict__ gthr) {
+    int64_t cap, int64_t N, int k, int64_t smax, int grid, uint32_t *__restrict__ gthr,
+    uint32_t *__restrict__ lvl) {
   __shared__ uint32_t vals[kSeedMax];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t sel[2];   // chosen digit, values above it
@@ -1209,6 +1304,10 @@ __global__ __launch_bounds__(kSeedThreads) void mfma_seed_kernel(
   const int64_t per = sp.S * kMLanesQ * seed_tiles(k, sp.ntiles, sp.S);
   const int n = (int)(per < kSeedMax ? per : kSeedMax);
   const int tid = threadIdx.x;
+  // no item of this call has finished yet: no published order statistics
+  for (int64_t e = (int64_t)blockIdx.x * kSeedThreads + tid; e < nu * kLvl * sp.S;
+       e += (int64_t)gridDim.x * kSeedThreads)
+    lvl[e] = 0u;
   if (n < k) {   // fewer lane maxima than k: no seed
     for (int64_t q = (int64_t)blockIdx.x * kSeedThreads + tid; q < nu;
          q += (int64_t)gridDim.x * kSeedThreads)
@@ -1274,6 +1373,8 @@ hipError_t launch_score_mfma(const void *q, const void *corpus, const float *sca
   // shared thresholds: (re)started by the seed selection on every call
   uint32_t *gthr = (uint32_t *)ws;
   uint32_t *lmax = (uint32_t *)((unsigned char *)ws + mfma_thr_bytes(cap));
+  uint32_t *lvl = (uint32_t *)((unsigned char *)ws + mfma_thr_bytes(cap) +
+                               mfma_lmax_bytes(cap, N, k, kMGridMax));
   void *part = (unsigned char *)ws + mfma_part_offset(cap, N, k, kMGridMax);
   MfmaArgs a;
   a.q = q;
@@ -1288,6 +1389,7 @@ hipError_t launch_score_mfma(const void *q, const void *corpus, const float *sca
   a.part = (uint64_t *)part;
   a.gthr = gthr;
   a.lmax = lmax;
+  a.lvl = lvl;
   a.grid = persistent_grid(true);
   // k-lists in LDS when they fit beside the ring
   const bool ll = mfma_lds_bytes(fp8, true, k) <= kMLdsMax;
@@ -1315,7 +1417,7 @@ hipError_t launch_score_mfma(const void *q, const void *corpus, const float *sca
     const int64_t blocks = want < 4 * (int64_t)a.grid ? want : 4 * (int64_t)a.grid;
     if (blocks > 0) {
       hipLaunchKernelGGL(mfma_seed_kernel, dim3((unsigned)blocks), dim3(kSeedThreads), 0, st,
-                         a.lmax, n_unique, nu_dev, cap, N, k, smax, a.grid, gthr);
+                         a.lmax, n_unique, nu_dev, cap, N, k, smax, a.grid, gthr, a.lvl);
       e = hipGetLastError();
       if (e != hipSuccess) return e;
     }
