@@ -47,12 +47,13 @@
 // blocks that reach it are examined, and their scores at or above it are
 // appended to a small per-query LDS queue (one atomic per lane and block
 // reserves the slots), merged into the query's sorted k-list when a queue
-// fills.  Thresholds come from three lower bounds of the query's final k-th
-// best score: the slice's own k-list; a seed, the k-th largest of the lane
-// maxima of a first pass over one tile of every slice (a sample spread over
-// the corpus); and the largest bound any slice of the query has published so
-// far (a per-query array in the workspace, read asynchronously with each
-// tile's copies).  Keys order by (score desc, row asc): ties go to the lower
+// is due.  Thresholds come from lower bounds of the query's final k-th best
+// score: the slice's own k-list; a seed, the k-th largest of the lane maxima
+// of a first pass over the first tiles of every slice (a sample spread over
+// the corpus); the order statistics of the slices finished so far; and the
+// largest bound any slice of the query has published so far (a per-query
+// array in the workspace, read asynchronously with each tile's copies).
+// Keys order by (score desc, row asc): ties go to the lower
 // corpus row independently of tile, slice or lane.
 #include <type_traits>
 
@@ -1403,9 +1404,9 @@ hipError_t launch_score_mfma(const void *q, const void *corpus, const float *sca
     return ll ? launch_mfma(score_mfma_dma<false, true, false>, a.grid, lds, a, st)
               : launch_mfma(score_mfma_dma<false, false, false>, a.grid, lds, a, st);
   };
-  // Seed pass: score the first tile of every slice and keep only lane
+  // Seed pass: score the first T tiles of every slice and keep only lane
   // maxima; their k-th largest per query (a lower bound of the query's k-th
-  // best over the corpus, taken over a sample of S tiles spread over it)
+  // best over the corpus, taken over a sample of S T tiles spread over it)
   // seeds the shared thresholds.  The main pass then scores every tile with
   // lists that stay nearly untouched from the first tile on.
   hipError_t e = run(true);
