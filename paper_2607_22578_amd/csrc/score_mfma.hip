@@ -55,6 +55,7 @@
 // array in the workspace, read asynchronously with each tile's copies).
 // Keys order by (score desc, row asc): ties go to the lower
 // corpus row independently of tile, slice or lane.
+#include <mutex>
 #include <type_traits>
 
 #include "common.h"
@@ -1223,9 +1224,31 @@ int persistent_grid(bool mfma);
 size_t mfma_thr_bytes(int64_t cap) { return ((size_t)cap * 4 + 255) & ~(size_t)255; }
 
 // worst case over n_u in [1, cap] and grids up to grid_max of n_u * S * f(k),
-// f(k) = per_slice bytes, times the seed pass's tiles per slice if seed
+// f(k) = per_slice bytes, times the seed pass's tiles per slice if seed.
+// It takes up to (cap / 128) x 64 splits, and every score call lays out its
+// workspace with it, so results are kept for the few shapes a process uses
+// (on a window of a few hundred queries the loops cost tens of microseconds,
+// on the launch path).
+struct SplitWorstMemo {
+  int64_t cap, N;
+  int k, grid_max;
+  size_t per_slice;
+  bool seed, valid;
+  size_t bytes;
+};
+static std::mutex g_split_memo_mu;
+static SplitWorstMemo g_split_memo[16];
+static unsigned g_split_memo_next = 0;
+
 static size_t mfma_split_worst(int64_t cap, int64_t N, int k, int grid_max, size_t per_slice,
                                bool seed = false) {
+  {
+    std::lock_guard<std::mutex> lock(g_split_memo_mu);
+    for (const SplitWorstMemo &m : g_split_memo)
+      if (m.valid && m.cap == cap && m.N == N && m.k == k && m.grid_max == grid_max &&
+          m.per_slice == per_slice && m.seed == seed)
+        return m.bytes;
+  }
   size_t best = 0;
   const int64_t qtmax = (cap + kMMQ - 1) / kMMQ;
   int64_t smax = kMSplitMaxSK / k;
@@ -1239,7 +1262,10 @@ static size_t mfma_split_worst(int64_t cap, int64_t N, int k, int grid_max, size
       if (b > best) best = b;
     }
   }
-  return (best + 255) & ~(size_t)255;
+  best = (best + 255) & ~(size_t)255;
+  std::lock_guard<std::mutex> lock(g_split_memo_mu);
+  g_split_memo[g_split_memo_next++ % 16] = {cap, N, k, grid_max, per_slice, seed, true, best};
+  return best;
 }
 
 // Score workspace of the matrix-core path: [shared thresholds, cap x u32 |
