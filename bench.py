@@ -125,6 +125,10 @@ def parse():
                     help="with --batch-curve: only the latency curve, at these comma-separated "
                          "batch sizes (default: the full curve 1,2,4,...,2048 and the sub-batch "
                          "and stream-split runs)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one window (dedup, gather, score, merge, delivery) as a HIP "
+                         "graph after the warm-up and time its replays (the score-step events "
+                         "then come from eager steps after the timed region)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
     return ap.parse_args()
@@ -250,6 +254,16 @@ def main():
         step()
     torch.cuda.synchronize(dev)
     n_u = int(m.n_unique.item())
+    graph = None
+    if args.graph:
+        if sig is not None or prio is not None or windows is not None:
+            raise SystemExit("--graph captures the plain window (no --signatures, "
+                             "--priorities or --reuse-store)")
+        # the window issues kernel launches only (device-side distinct count)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            step()
+        torch.cuda.synchronize(dev)
 
     # The score step is timed with HIP events on its stream inside the timed
     # region, on every EV_EVERY-th step: each timing event costs the stream
@@ -267,13 +281,22 @@ def main():
     torch.cuda.synchronize(dev)
     wall0 = time.perf_counter()
     t_start.record(stream)
-    for i in range(args.steps):
-        step(evs.get(i))
+    if graph is not None:
+        with torch.cuda.stream(stream):
+            for i in range(args.steps):
+                graph.replay()
+    else:
+        for i in range(args.steps):
+            step(evs.get(i))
     t_end.record(stream)
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - wall0
     total_ms = t_start.elapsed_time(t_end)
     ms_per_step = total_ms / args.steps
+    if graph is not None:   # score-step events from eager steps (outside the timed region)
+        for i in ev_steps:
+            step(evs[i])
+        torch.cuda.synchronize(dev)
     kern_samples = np.array([a.elapsed_time(b) for a, b in evs.values()])
     kern_ms = float(np.mean(kern_samples))
 
@@ -388,7 +411,8 @@ def main():
                    "corpus_dtype": cfg.c_enc, "seed": w.seed,
                    "merge": not args.no_merge, "reuse": reuse,
                    "signatures": args.signatures, "priorities": args.priorities,
-                   "raw_ids": args.raw_ids, "dedup_path": dedup_path(w.keys)},
+                   "raw_ids": args.raw_ids, "dedup_path": dedup_path(w.keys),
+                   "graph": args.graph},
         "unique_queries_per_s": round(n_distinct * args.steps / (total_ms * 1e-3), 1),
         "stages_ms": stages,
         "wall_s_timed": round(wall, 4),
