@@ -3,8 +3,9 @@ the oracle (acceptance rule of oracle/accept.py): dimensions that leave a
 partial last K stage (the copies read zeros past d), corpora smaller than
 one 384-row tile or with a ragged last tile, k-lists held in global memory
 instead of LDS, k too large for the first-pass threshold seed, a seed that
-samples several tiles per slice (k > 48), and a merge with more survivors
-than it ranks by counting (it sorts them)."""
+samples several tiles per slice (k > 48), items of later rounds that start
+from the order statistics of finished slices, and a merge with more
+survivors than it ranks by counting (it sorts them)."""
 import numpy as np
 import pytest
 
@@ -98,4 +99,29 @@ def test_large_k_seed_samples_several_tiles(enc):
     ref = check_dedup(m, w.keys)
     sel = np.random.default_rng(11).choice(ref["n_unique"], size=40, replace=False)
     check_unique_topk(m, ref, q, c, k, scale=sc if enc == "fp8" else None, sel=np.sort(sel))
+    check_delivery(m, w.R)
+
+
+@pytest.mark.parametrize("enc", ["bf16", "fp8"])
+def test_thresholds_from_finished_slices(enc):
+    # k = 64 over 350,000 rows (912 tiles) for the 20M-row workload's request
+    # stream (2,197 distinct queries, 18 query tiles): 71 slices of ~13 tiles,
+    # 1,278 items in five rounds of the 256-workgroup grid, so items of
+    # rounds 2-5 start from the order statistics that the finished slices
+    # published (k-lists in global memory)
+    w = synth.make("fp8_20m", n_corpus=1, with_corpus=False)
+    d, n_corpus, k = 64, 350_000, 64
+    q, _ = synth.gaussian_rows(w.seed, synth.S_QUERY, 0, d, "bf16", row_ids=w.template_ids)
+    c, sc = synth.gaussian_rows(w.seed, synth.S_CORPUS, n_corpus, d, enc)
+    scale = sc if enc == "fp8" else None
+    note(f"{enc} k={k} N={n_corpus} d={d}: five rounds")
+    m = run_merge(w.keys, q, c, k, scale=scale)
+    ref = check_dedup(m, w.keys)
+    nu = ref["n_unique"]
+    # eight queries of every query tile, and the first and last
+    rng = np.random.default_rng(5)
+    sel = [0, nu - 1]
+    for b0 in range(0, nu, 128):
+        sel.extend((b0 + rng.choice(min(128, nu - b0), size=8, replace=False)).tolist())
+    check_unique_topk(m, ref, q, c, k, scale=scale, sel=np.unique(np.array(sel)))
     check_delivery(m, w.R)
