@@ -318,8 +318,13 @@ def main():
                  "hit_frac": round(1.0 - float(nms.sum()) / max(int(nus.sum()), 1), 4)}
         n_u = float(nms.mean())   # queries the score step processes per window
         n_distinct = float(nus.mean())
+        # the windows whose score steps the events timed: a window whose keys
+        # all hit the store scores nothing and moves no corpus bytes
+        timed_miss = nms[np.array(ev_steps)]
+        reuse_pricing = (float(timed_miss.mean()), float((timed_miss > 0).mean()))
     else:
         n_distinct = n_u
+        reuse_pricing = None
 
     # stage breakdown (separate, untimed-for-value pass)
     st_ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
@@ -356,9 +361,13 @@ def main():
     # roofline of the scoring kernel: algorithmic work per launch
     c_bytes = N * d * {"fp8": 1, "bf16": 2, "f32": 4}[cfg.c_enc] + \
         (N * 4 if cfg.c_enc == "fp8" else 0)
-    q_bytes = n_u * d * (4 if f32 else 2)
+    n_q = n_u
+    if reuse_pricing is not None:   # mean over the timed windows
+        n_q, scored = reuse_pricing
+        c_bytes *= scored
+    q_bytes = n_q * d * (4 if f32 else 2)
     alg_bytes = c_bytes + q_bytes
-    alg_flops = 2.0 * n_u * N * d
+    alg_flops = 2.0 * n_q * N * d
     t_s = kern_ms * 1e-3
     tflops = alg_flops / t_s / 1e12
     gbs = alg_bytes / t_s / 1e9
@@ -390,7 +399,8 @@ def main():
     src_hash = kernel_source_hash()
     roof["kernel_source"] = src_hash
     if windows is not None:
-        roof["note"] = "reuse mode: score-step work priced at the mean miss count"
+        roof["note"] = ("reuse mode: score-step work priced over the timed windows (their mean "
+                        "miss count; corpus bytes only where a window has a miss)")
     tf = traffic_file(args.workload)
     if not (args.no_merge or args.raw_ids or args.corpus_rows or windows is not None
             or args.seed is not None) and os.path.exists(tf):
