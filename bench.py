@@ -129,6 +129,10 @@ def parse():
                     help="capture one window (dedup, gather, score, merge, delivery) as a HIP "
                          "graph after the warm-up and time its replays (the score-step events "
                          "then come from eager steps after the timed region)")
+    ap.add_argument("--corpus-layout", choices=("tiled", "rows"), default="tiled",
+                    help="storage of a BF16/FP8 corpus: tiled (default; hs_tile_corpus, made "
+                         "once before the warm-up, as an index is) or row-major (rows); an "
+                         "F32 corpus is always row-major")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
     return ap.parse_args()
@@ -199,8 +203,13 @@ def main():
 
     keys, q_req, corpus = to_dev(w.keys), to_dev(w.q_req), to_dev(w.corpus)
     scale = to_dev(w.scale) if w.scale is not None else None
-    m = hs.MergedRetrieval(R, d, N, k, qdt, cdt, device=dev)
+    tiled = args.corpus_layout == "tiled" and not f32
+    m = hs.MergedRetrieval(R, d, N, k, qdt, cdt, device=dev, tiled_corpus=tiled)
     stream = torch.cuda.Stream(dev)   # default priority
+    if tiled:
+        # the corpus is the retrieval index: laid out once, before any timing
+        corpus = m.tile_corpus(corpus, stream)
+        torch.cuda.synchronize(dev)
     sig = None
     if args.signatures:
         if args.no_merge:
@@ -403,7 +412,8 @@ def main():
                         "miss count; corpus bytes only where a window has a miss)")
     tf = traffic_file(args.workload)
     if not (args.no_merge or args.raw_ids or args.corpus_rows or windows is not None
-            or args.seed is not None) and os.path.exists(tf):
+            or args.seed is not None or (args.corpus_layout == "rows" and not f32)) \
+            and os.path.exists(tf):
         tr = json.load(open(tf))
         if tr.get("kernel_source") == src_hash:
             roof["traffic"] = tr.get("hbm_bytes_per_launch")
@@ -422,7 +432,7 @@ def main():
                    "merge": not args.no_merge, "reuse": reuse,
                    "signatures": args.signatures, "priorities": args.priorities,
                    "raw_ids": args.raw_ids, "dedup_path": dedup_path(w.keys),
-                   "graph": args.graph},
+                   "graph": args.graph, "corpus_layout": "tiled" if tiled else "rows"},
         "unique_queries_per_s": round(n_distinct * args.steps / (total_ms * 1e-3), 1),
         "stages_ms": stages,
         "wall_s_timed": round(wall, 4),
@@ -635,8 +645,12 @@ def batch_curve_bench(args):
 
     keys, q_req, corpus = to_dev(w.keys), to_dev(w.q_req), to_dev(w.corpus)
     scale = to_dev(w.scale) if w.scale is not None else None
-    m = hs.MergedRetrieval(R, d, N, k, hs.HS_BF16, cdt, device=dev)
+    tiled = args.corpus_layout == "tiled"
+    m = hs.MergedRetrieval(R, d, N, k, hs.HS_BF16, cdt, device=dev, tiled_corpus=tiled)
     stream = torch.cuda.Stream(dev)
+    if tiled:
+        corpus = m.tile_corpus(corpus, stream)
+        torch.cuda.synchronize(dev)
     nu = m.dedup(keys, stream, host_count=True)
     reps = max(3, min(args.steps, 20))
 
@@ -673,7 +687,8 @@ def batch_curve_bench(args):
                "n_gpus": 1, "steps": reps, "warmup": 2, "ms_per_step": worst["ms"],
                "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
                "dtype": "bf16", "data": "synthetic",
-               "config": {"workload": f"{cfg.name}: {cfg.desc}", "k": k, "n_corpus": N},
+               "config": {"workload": f"{cfg.name}: {cfg.desc}", "k": k, "n_corpus": N,
+                          "corpus_layout": "tiled" if tiled else "rows"},
                "latency_curve": curve}
         print(json.dumps(out), flush=True)
         return
@@ -729,7 +744,7 @@ def batch_curve_bench(args):
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic",
            "config": {"workload": f"{cfg.name}: {cfg.desc}", "n_unique": nu, "k": k,
-                      "n_corpus": N},
+                      "n_corpus": N, "corpus_layout": "tiled" if tiled else "rows"},
            "latency_curve": curve, "sequential_sub_batches": chunked, "stream_split": split}
     print(json.dumps(out), flush=True)
 

@@ -40,7 +40,8 @@
  *     All work is asynchronous on that stream; outputs are valid after the
  *     stream is synchronised.  The only host synchronisation the library ever
  *     performs is the optional n_unique_host readback of hs_dedup.
- *   - Layout: row-major and contiguous.  Row data pointers must be 16-byte
+ *   - Layout: row-major and contiguous (a BF16/FP8 corpus may instead be in
+ *     the tiled layout of hs_tile_corpus).  Row data pointers must be 16-byte
  *     aligned; integer arrays must be aligned to their element size.
  *   - Device-side faults (e.g. an out-of-range index inside device data) cannot
  *     be reported synchronously: kernels skip such entries instead of reading
@@ -56,7 +57,7 @@
 extern "C" {
 #endif
 
-#define HS_ABI_VERSION 2
+#define HS_ABI_VERSION 3
 
 typedef enum {
     HS_OK = 0,
@@ -84,7 +85,9 @@ typedef struct {
     int32_t query_dtype;  /* HS_F32 or HS_BF16 */
     int32_t corpus_dtype; /* HS_F32 (with F32 queries), HS_BF16 or HS_FP8_E4M3
                              (with BF16 queries) */
-    int32_t flags;        /* reserved, must be 0 */
+    int32_t flags;        /* 0 or HS_FLAG_TILED_CORPUS (BF16/FP8 corpora only):
+                             the corpus argument of the score calls is then
+                             the tiled copy made by hs_tile_corpus */
     int64_t max_unique;   /* batch limit B_r of Appendix A (0 = n_requests): the
                              score step handles at most this many distinct
                              queries per call; a window with more distinct keys
@@ -101,6 +104,9 @@ typedef struct {
                              n_requests and every workflow has n_requests / W.
                              Read and copied during hs_merge_plan only. */
 } hs_merge_desc;
+
+/* hs_merge_desc.flags: the score calls read the corpus in the tiled layout. */
+#define HS_FLAG_TILED_CORPUS 1
 
 typedef struct hs_plan hs_plan;   /* opaque, immutable, thread-safe host object */
 
@@ -148,7 +154,8 @@ hs_status hs_dedup(const hs_plan *plan, const int64_t *keys, int64_t *unique_key
  *   n_unique      host count n_u, or -1 to read it from n_unique_dev on the
  *                 device (the launch then covers max_unique rows)
  *   n_unique_dev  int64 device, used when n_unique == -1 (else may be NULL)
- *   corpus        [N x d] device, corpus_dtype
+ *   corpus        [N x d] device, corpus_dtype; with HS_FLAG_TILED_CORPUS the
+ *                 tiled copy of it (hs_tile_corpus), same scores and results
  *   row_scale     [N] fp32 device: per-row dequantisation scale, FP8 only
  *                 (score = row_scale[c] * <q, decode(C[c])>), else NULL
  *   topk_score    [n_u x k] fp32 device out: best scores, descending
@@ -185,6 +192,27 @@ hs_status hs_score_topk_noalloc(const hs_plan *plan, const void *q_unique, int64
                                 const int64_t *n_unique_dev, const void *corpus,
                                 const float *row_scale, float *topk_score, int32_t *topk_index,
                                 void *stream);
+
+/* Storage layout of a BF16 or FP8 corpus for the score calls (not a step of the
+ * method: the corpus of the retrieval nodes, Sec. 3.3 (I) / Sec. 4.1, stored in
+ * the order the score kernel copies it, so that each copy reads consecutive
+ * bytes; scores and results are the same as from the row-major corpus).
+ * Blocks of 384 rows x 64 columns, block (t, s) at byte (t * ceil(d / 64) + s)
+ * * 384 * 64 * esz (esz = 2 for BF16, 1 for FP8), each block row-major with the
+ * 16-byte pieces of row r permuted within the row (piece p in slot p XOR a
+ * function of r mod 16); rows past N and columns past d hold zeros.  A corpus
+ * is tiled once and scored in any number of windows.
+ * hs_corpus_tiled_bytes: *bytes = size of the tiled copy for the plan's
+ *   corpus shape (ceil(N / 384) * 384 * ceil(d / 64) * 64 * esz);
+ *   HS_ERR_UNSUPPORTED for an F32 corpus.
+ * hs_tile_corpus: writes the tiled copy of `corpus` ([N x d] row-major device,
+ *   corpus_dtype) to `tiled` (device, tiled_bytes >= hs_corpus_tiled_bytes,
+ *   not overlapping `corpus`; both 16-byte aligned), asynchronously on
+ *   `stream`.  The plan's flags need not include HS_FLAG_TILED_CORPUS; plans
+ *   that score the tiled copy must. */
+hs_status hs_corpus_tiled_bytes(const hs_plan *plan, size_t *bytes);
+hs_status hs_tile_corpus(const hs_plan *plan, const void *corpus, void *tiled,
+                         size_t tiled_bytes, void *stream);
 
 /* Phase 1 of hs_score_topk: scores every distinct query against the corpus in
  * one persistent kernel, each workgroup keeping the k best (score, row) pairs

@@ -33,14 +33,16 @@ _lib = ctypes.CDLL(LIB_PATH)
 HS_OK, HS_ERR_INVALID_ARG, HS_ERR_UNSUPPORTED, HS_ERR_WORKSPACE, HS_ERR_ALIGNMENT, \
     HS_ERR_DEVICE = range(6)
 HS_F32, HS_BF16, HS_FP8_E4M3 = 0, 1, 2
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 EXPORTS = ["hs_merge_plan", "hs_plan_destroy", "hs_workflow_rows", "hs_dedup", "hs_score_topk",
-           "hs_score_topk_noalloc", "hs_score_partial", "hs_topk_merge", "hs_scatter", "hs_deliver",
+           "hs_score_topk_noalloc", "hs_score_partial", "hs_topk_merge", "hs_corpus_tiled_bytes",
+           "hs_tile_corpus", "hs_scatter", "hs_deliver",
            "hs_cache_bytes", "hs_cache_reset", "hs_cache_lookup",
            "hs_cache_insert", "hs_signature", "hs_priority", "hs_status_string",
            "hs_last_error", "hs_abi_version"]
 HS_SIG_NORMALIZE_TEXT = 1
+HS_FLAG_TILED_CORPUS = 1
 
 
 class hs_merge_desc(ctypes.Structure):
@@ -81,6 +83,10 @@ _lib.hs_score_partial.argtypes = [_vp, _vp, _i64, _vp, _vp, _vp, _vp, _sz, _vp]
 _lib.hs_score_partial.restype = ctypes.c_int
 _lib.hs_topk_merge.argtypes = [_vp, _i64, _vp, _vp, _vp, _vp, _sz, _vp]
 _lib.hs_topk_merge.restype = ctypes.c_int
+_lib.hs_corpus_tiled_bytes.argtypes = [_vp, ctypes.POINTER(_sz)]
+_lib.hs_corpus_tiled_bytes.restype = ctypes.c_int
+_lib.hs_tile_corpus.argtypes = [_vp, _vp, _vp, _sz, _vp]
+_lib.hs_tile_corpus.restype = ctypes.c_int
 _lib.hs_scatter.argtypes = [_vp, _i64, _i64, _vp, _i32, _i64, _vp, _vp, _vp]
 _lib.hs_scatter.restype = ctypes.c_int
 _lib.hs_cache_bytes.argtypes = [_vp, _i64, ctypes.POINTER(_sz)]
@@ -229,6 +235,19 @@ def hs_score_topk(plan: Plan, q_unique, n_unique: int, n_unique_dev, corpus, row
                               _ptr(ws), _ws_bytes(ws, ws_bytes), _stream(stream)))
 
 
+def hs_corpus_tiled_bytes(plan: Plan) -> int:
+    n = _sz()
+    _check(_lib.hs_corpus_tiled_bytes(plan.handle, ctypes.byref(n)))
+    return int(n.value)
+
+
+def hs_tile_corpus(plan: Plan, corpus, tiled, tiled_bytes: Optional[int] = None, stream=None):
+    if tiled_bytes is None:
+        tiled_bytes = tiled.numel() * tiled.element_size() if tiled is not None else 0
+    _check(_lib.hs_tile_corpus(plan.handle, _ptr(corpus), _ptr(tiled), tiled_bytes,
+                               _stream(stream)))
+
+
 def hs_score_topk_noalloc(plan: Plan, q_unique, n_unique: int, n_unique_dev, corpus, row_scale,
                           topk_score, topk_index, stream=None):
     _check(_lib.hs_score_topk_noalloc(plan.handle, _ptr(q_unique), n_unique, _ptr(n_unique_dev),
@@ -326,12 +345,16 @@ class MergedRetrieval:
 
     def __init__(self, n_requests: int, dim: int, n_corpus: int, k: int, query_dtype: int,
                  corpus_dtype: int, device="cuda", max_unique: int = 0, n_workflows: int = 1,
-                 workflow_offsets=None):
+                 workflow_offsets=None, tiled_corpus: bool = False):
+        """tiled_corpus: the score calls take the corpus in the tiled layout
+        (make it once with tile_corpus)."""
         import torch
         self.R, self.d, self.N, self.k = n_requests, dim, n_corpus, k
         self.qdt, self.cdt = query_dtype, corpus_dtype
+        self.tiled_corpus = tiled_corpus
         self.plan = hs_merge_plan(n_requests, dim, n_corpus, k, query_dtype, corpus_dtype,
-                                  max_unique, n_workflows=n_workflows,
+                                  max_unique, flags=HS_FLAG_TILED_CORPUS if tiled_corpus else 0,
+                                  n_workflows=n_workflows,
                                   workflow_offsets=workflow_offsets)
         self.n_workflows = n_workflows
         cap = max_unique if max_unique > 0 else n_requests
@@ -353,6 +376,15 @@ class MergedRetrieval:
         self.out_score = torch.empty((R1, k), dtype=torch.float32, device=dev)
         self.out_index = torch.empty((R1, k), dtype=torch.int32, device=dev)
         self.q_row_bytes = dim * (4 if query_dtype == HS_F32 else 2)
+
+    def tile_corpus(self, corpus, stream=None):
+        """The tiled copy of a row-major BF16/FP8 corpus (a new device tensor),
+        for a MergedRetrieval made with tiled_corpus=True."""
+        import torch
+        out = torch.empty(max(hs_corpus_tiled_bytes(self.plan), 16), dtype=torch.uint8,
+                          device=corpus.device)
+        hs_tile_corpus(self.plan, corpus, out, stream=stream)
+        return out
 
     def dedup(self, keys, stream=None, host_count: bool = False):
         return hs_dedup(self.plan, keys, self.unique_keys, self.first_index, self.counts,

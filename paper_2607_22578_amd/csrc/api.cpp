@@ -29,7 +29,11 @@ hipError_t noalloc_scratch(void **ptr);
 size_t score_workspace_bytes(int64_t cap, int64_t N, int k, int corpus_dtype);
 hipError_t launch_score_partial(const void *q, const void *corpus, const float *scale, int64_t N,
                                 int64_t d, int k, int64_t n_unique, const int64_t *nu_dev,
-                                int64_t cap, int corpus_dtype, void *part, hipStream_t st);
+                                int64_t cap, int corpus_dtype, bool tiled, void *part,
+                                hipStream_t st);
+size_t mfma_tiled_bytes(int64_t N, int64_t d, bool fp8);
+hipError_t launch_tile_corpus(const void *corpus, int64_t N, int64_t d, bool fp8, void *tiled,
+                              hipStream_t st);
 hipError_t launch_topk_merge(const void *part, int64_t n_unique, const int64_t *nu_dev,
                              int64_t cap, int64_t N, int k, int corpus_dtype, float *out_s,
                              int32_t *out_i, hipStream_t st);
@@ -111,7 +115,8 @@ hs_status hs_merge_plan(const hs_merge_desc *desc, hs_plan **plan, size_t *works
   if (!desc || !plan || !workspace_bytes)
     return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: null argument");
   const hs_merge_desc &d = *desc;
-  if (d.flags != 0) return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: flags must be 0");
+  if ((d.flags & ~HS_FLAG_TILED_CORPUS) != 0)
+    return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: unknown flags 0x%x", d.flags);
   // (2^30 keeps every request index and tile offset of the kernels' int32
   // arithmetic far from overflow)
   if (d.n_requests < 0 || d.n_requests > ((int64_t)1 << 30))
@@ -141,6 +146,8 @@ hs_status hs_merge_plan(const hs_merge_desc *desc, hs_plan **plan, size_t *works
     return fail(HS_ERR_UNSUPPORTED, "hs_merge_plan: BF16 needs dim %% 8 == 0");
   if (d.corpus_dtype == HS_FP8_E4M3 && d.dim % 16 != 0)
     return fail(HS_ERR_UNSUPPORTED, "hs_merge_plan: FP8 corpus needs dim %% 16 == 0");
+  if ((d.flags & HS_FLAG_TILED_CORPUS) && d.corpus_dtype == HS_F32)
+    return fail(HS_ERR_UNSUPPORTED, "hs_merge_plan: the tiled layout is for BF16/FP8 corpora");
   if (d.n_workflows < 1 || d.n_workflows > ((int64_t)1 << 30))
     return fail(HS_ERR_INVALID_ARG, "hs_merge_plan: n_workflows %lld out of [1, 2^30]",
                 (long long)d.n_workflows);
@@ -273,7 +280,8 @@ hs_status hs_score_partial(const hs_plan *plan, const void *q_unique, int64_t n_
   if (s != HS_OK) return s;
   const hs_merge_desc &d = plan->d;
   hipError_t e = hs::launch_score_partial(q_unique, corpus, row_scale, d.n_corpus, d.dim, d.k,
-                                          n_unique, n_unique_dev, plan->cap, d.corpus_dtype, ws,
+                                          n_unique, n_unique_dev, plan->cap, d.corpus_dtype,
+                                          (d.flags & HS_FLAG_TILED_CORPUS) != 0, ws,
                                           (hipStream_t)stream);
   return device_status(e, "hs_score_partial launch");
 }
@@ -348,11 +356,49 @@ hs_status hs_score_topk_noalloc(const hs_plan *plan, const void *q_unique, int64
   if (e != hipSuccess) return device_status(e, "hs_score_topk_noalloc scratch");
   hipStream_t st = (hipStream_t)stream;
   e = hs::launch_score_partial(q_unique, corpus, row_scale, d.n_corpus, d.dim, d.k, n_unique,
-                               n_unique_dev, plan->cap, d.corpus_dtype, ws, st);
+                               n_unique_dev, plan->cap, d.corpus_dtype,
+                               (d.flags & HS_FLAG_TILED_CORPUS) != 0, ws, st);
   if (e != hipSuccess) return device_status(e, "hs_score_topk_noalloc launch");
   e = hs::launch_topk_merge(ws, n_unique, n_unique_dev, plan->cap, d.n_corpus, d.k,
                             d.corpus_dtype, topk_score, topk_index, st);
   return device_status(e, "hs_score_topk_noalloc launch");
+}
+
+hs_status hs_corpus_tiled_bytes(const hs_plan *plan, size_t *bytes) {
+  if (!plan || !bytes) return fail(HS_ERR_INVALID_ARG, "hs_corpus_tiled_bytes: null argument");
+  const hs_merge_desc &d = plan->d;
+  if (d.corpus_dtype == HS_F32)
+    return fail(HS_ERR_UNSUPPORTED, "hs_corpus_tiled_bytes: the tiled layout is for BF16/FP8 "
+                "corpora");
+  *bytes = hs::mfma_tiled_bytes(d.n_corpus, d.dim, d.corpus_dtype == HS_FP8_E4M3);
+  return HS_OK;
+}
+
+hs_status hs_tile_corpus(const hs_plan *plan, const void *corpus, void *tiled,
+                         size_t tiled_bytes, void *stream) {
+  size_t need = 0;
+  hs_status s = hs_corpus_tiled_bytes(plan, &need);
+  if (s != HS_OK) return s;
+  const hs_merge_desc &d = plan->d;
+  if (!corpus && d.n_corpus > 0) return fail(HS_ERR_INVALID_ARG, "hs_tile_corpus: null corpus");
+  if (!tiled && need > 0) return fail(HS_ERR_INVALID_ARG, "hs_tile_corpus: null tiled buffer");
+  if (tiled_bytes < need)
+    return fail(HS_ERR_INVALID_ARG, "hs_tile_corpus: tiled buffer of %zu bytes, %zu needed",
+                tiled_bytes, need);
+  if (!aligned(corpus, 16) || !aligned(tiled, 16))
+    return fail(HS_ERR_ALIGNMENT, "hs_tile_corpus: corpus/tiled must be 16-byte aligned");
+  if (corpus && tiled && need > 0) {
+    // the source rows and the tiled buffer must not overlap
+    const uintptr_t c0 = (uintptr_t)corpus, t0 = (uintptr_t)tiled;
+    const size_t cb = (size_t)d.n_corpus * (size_t)d.dim *
+                      (d.corpus_dtype == HS_FP8_E4M3 ? 1u : 2u);
+    if (c0 < t0 + need && t0 < c0 + cb)
+      return fail(HS_ERR_INVALID_ARG, "hs_tile_corpus: corpus and tiled buffer overlap");
+  }
+  hipError_t e = hs::launch_tile_corpus(corpus, d.n_corpus, d.dim,
+                                        d.corpus_dtype == HS_FP8_E4M3, tiled,
+                                        (hipStream_t)stream);
+  return device_status(e, "hs_tile_corpus launch");
 }
 
 hs_status hs_scatter(const void *src, int64_t src_rows, int64_t row_bytes, const void *index,

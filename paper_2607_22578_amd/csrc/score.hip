@@ -500,7 +500,7 @@ size_t mfma_part_offset(int64_t cap, int64_t N, int k, int grid_max);
 void mfma_split_params(int *mq, int *nc, int64_t *smax, int k);
 hipError_t launch_score_mfma(const void *q, const void *corpus, const float *scale, int64_t N,
                              int64_t d, int k, int64_t n_unique, const int64_t *nu_dev,
-                             int64_t cap, bool fp8, void *ws, hipStream_t st);
+                             int64_t cap, bool fp8, bool tiled, void *ws, hipStream_t st);
 
 static size_t partial_bytes(int64_t cap, int64_t N, int mq, int nc, int k) {
   // worst case over n_u in [1, cap] of n_u * S(n_u) * k keys, for any grid
@@ -535,10 +535,11 @@ static hipError_t launch_with_lds(K kern, int grid, int threads, int lds, const 
 
 hipError_t launch_score_partial(const void *q, const void *corpus, const float *scale, int64_t N,
                                 int64_t d, int k, int64_t n_unique, const int64_t *nu_dev,
-                                int64_t cap, int corpus_dtype, void *part, hipStream_t st) {
+                                int64_t cap, int corpus_dtype, bool tiled, void *part,
+                                hipStream_t st) {
   if (corpus_dtype != HS_F32)
     return launch_score_mfma(q, corpus, scale, N, d, k, n_unique, nu_dev, cap,
-                             corpus_dtype == HS_FP8_E4M3, part, st);
+                             corpus_dtype == HS_FP8_E4M3, tiled, part, st);
   ScoreArgs a;
   a.q = q;
   a.corpus = corpus;

@@ -262,6 +262,7 @@ struct MfmaArgs {
   const int64_t *n_unique_dev;
   int64_t cap;
   int grid;
+  int tiled;        // corpus in the tiled layout (tile_corpus_kernel), else row-major
   uint64_t *part;
   uint32_t *gthr;   // [cap] per-query shared thresholds (ordered score, 0 = none)
   uint32_t *lmax;   // [n_u][S][T][8] lane maxima of the seed pass (ordered scores)
@@ -949,27 +950,36 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
     };
     auto prep_a = [&]() __attribute__((always_inline)) {
       CopyA ca;
-      const int row0 = (t0 + i_tl) * kMNC;
-      const int rows = N - row0 < kMNC ? N - row0 : kMNC;
-      ca.rs = make_rsrc((const unsigned char *)a.corpus + (int64_t)row0 * d * G::esz,
-                        (uint32_t)(rows * d * G::esz));
       unsigned char *st = L.ring + i_slot * G::stage;
       const int ln = opaque(lane);
       constexpr int PA = G::apieces;
       const int wvs = __builtin_amdgcn_readfirstlane(wv);
+      ca.lds = (uint32_t)(uintptr_t)st + wvs * G::adma * 1024;
+      if (a.tiled) {
+        // the tile's stages are consecutive blocks already in LDS order: this
+        // wave's copies read adma consecutive KiB of the stage's block
+        const uint32_t tb = (uint32_t)(nch * G::abytes);
+        ca.rs = make_rsrc((const unsigned char *)a.corpus + (int64_t)(t0 + i_tl) * tb, tb);
+        ca.voff = (uint32_t)((i_kc / kMKC) * G::abytes + wvs * G::adma * 1024 + ln * 16);
+        ca.voff1 = ca.voff;
+        return ca;
+      }
+      const int row0 = (t0 + i_tl) * kMNC;
+      const int rows = N - row0 < kMNC ? N - row0 : kMNC;
+      ca.rs = make_rsrc((const unsigned char *)a.corpus + (int64_t)row0 * d * G::esz,
+                        (uint32_t)(rows * d * G::esz));
       const int arow0 = wvs * G::adma * (64 / PA) + ln / PA;
       ca.voff = (uint32_t)(arow0 * d * G::esz + swz_slot<PA>(ln % PA, ln / PA) * 16 + i_kc * G::esz);
       // the swizzle depends on the row mod 16: a bf16 copy holds 8 rows, so odd
       // copies hold rows 8..15 mod 16 (an fp8 copy holds 16 rows: one pattern)
       ca.voff1 = (uint32_t)(arow0 * d * G::esz +
                             swz_slot<PA>(ln % PA, (64 / PA) % 16 + ln / PA) * 16 + i_kc * G::esz);
-      ca.lds = (uint32_t)(uintptr_t)st + wvs * G::adma * 1024;
       return ca;
     };
     auto issue_a_j = [&](const CopyA &ca, int j) __attribute__((always_inline)) {
       constexpr int PA = G::apieces;
-      dma16s(ca.rs, ca.lds + j * 1024,
-             ((j & 1) ? ca.voff1 : ca.voff) + (uint32_t)(j * (64 / PA) * d * G::esz));
+      const uint32_t jstep = a.tiled ? 1024u : (uint32_t)((64 / PA) * d * G::esz);
+      dma16s(ca.rs, ca.lds + j * 1024, ((j & 1) ? ca.voff1 : ca.voff) + (uint32_t)j * jstep);
     };
     auto issue_a = [&]() __attribute__((always_inline)) {
       if (i_left <= 0) return;
@@ -1394,9 +1404,63 @@ __global__ __launch_bounds__(kSeedThreads) void mfma_seed_kernel(
   }
 }
 
+// Tiled corpus layout.  Tile t (corpus rows [384 t, 384 t + 384)) and stage s
+// (columns [64 s, 64 s + 64)) form one block of Geo::abytes bytes at
+// (t * nch + s) * Geo::abytes, nch = ceil(d / 64): the stage exactly as the
+// copies place it in LDS, row r of the tile at r * Geo::arow with its 16-byte
+// pieces in the swizzled slots the fragment reads expect (slot x of row r holds
+// piece swz_slot(x, r)).  Rows past N and columns past d are zeros.  The score
+// kernel then copies each wave's share of a stage as consecutive KiB instead of
+// 8 (bf16) or 16 (fp8) row pieces per copy.
+template <bool FP8>
+__global__ __launch_bounds__(256) void tile_corpus_kernel(const unsigned char *__restrict__ src,
+                                                          int64_t N, int64_t d, int nch,
+                                                          int64_t npieces,
+                                                          uint4 *__restrict__ dst) {
+  using G = Geo<FP8>;
+  constexpr int PA = G::apieces;
+  constexpr int per_stage = G::abytes / 16;
+  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < npieces;
+       p += (int64_t)gridDim.x * 256) {
+    const int64_t blk = p / per_stage;
+    const int in = (int)(p - blk * per_stage);
+    const int64_t t = blk / nch;
+    const int s = (int)(blk - t * nch);
+    const int r = in / PA;
+    const int piece = swz_slot<PA>(in % PA, r);   // (an XOR: slot -> piece)
+    const int64_t row = t * kMNC + r;
+    const int64_t col = (int64_t)s * kMKC + piece * (16 / G::esz);
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (row < N && col < d)
+      v = *reinterpret_cast<const uint4 *>(src + (row * d + col) * G::esz);
+    dst[p] = v;
+  }
+}
+
+size_t mfma_tiled_bytes(int64_t N, int64_t d, bool fp8) {
+  const int64_t tiles = (N + kMNC - 1) / kMNC, nch = (d + kMKC - 1) / kMKC;
+  return (size_t)(tiles * nch) * (size_t)(fp8 ? Geo<true>::abytes : Geo<false>::abytes);
+}
+
+hipError_t launch_tile_corpus(const void *corpus, int64_t N, int64_t d, bool fp8, void *tiled,
+                              hipStream_t st) {
+  const int64_t npieces = (int64_t)(mfma_tiled_bytes(N, d, fp8) / 16);
+  if (npieces == 0) return hipSuccess;
+  const int nch = (int)((d + kMKC - 1) / kMKC);
+  const int64_t want = (npieces + 255) / 256;
+  const unsigned blocks = (unsigned)(want < 8192 ? want : 8192);
+  if (fp8)
+    hipLaunchKernelGGL(tile_corpus_kernel<true>, dim3(blocks), dim3(256), 0, st,
+                       (const unsigned char *)corpus, N, d, nch, npieces, (uint4 *)tiled);
+  else
+    hipLaunchKernelGGL(tile_corpus_kernel<false>, dim3(blocks), dim3(256), 0, st,
+                       (const unsigned char *)corpus, N, d, nch, npieces, (uint4 *)tiled);
+  return hipGetLastError();
+}
+
 hipError_t launch_score_mfma(const void *q, const void *corpus, const float *scale, int64_t N,
                              int64_t d, int k, int64_t n_unique, const int64_t *nu_dev,
-                             int64_t cap, bool fp8, void *ws, hipStream_t st) {
+                             int64_t cap, bool fp8, bool tiled, void *ws, hipStream_t st) {
   // shared thresholds: (re)started by the seed selection on every call
   uint32_t *gthr = (uint32_t *)ws;
   uint32_t *lmax = (uint32_t *)((unsigned char *)ws + mfma_thr_bytes(cap));
@@ -1418,6 +1482,7 @@ hipError_t launch_score_mfma(const void *q, const void *corpus, const float *sca
   a.lmax = lmax;
   a.lvl = lvl;
   a.grid = persistent_grid(true);
+  a.tiled = tiled ? 1 : 0;
   // k-lists in LDS when they fit beside the ring
   const bool ll = mfma_lds_bytes(fp8, true, k) <= kMLdsMax;
   const int lds = mfma_lds_bytes(fp8, ll, k);

@@ -39,18 +39,22 @@ def enc_code(a: np.ndarray) -> int:
             np.dtype(np.uint8): hs.HS_FP8_E4M3}[a.dtype]
 
 
-def run_merge(keys, q_req, corpus, k, scale=None, n_unique_mode="device", max_unique=0):
+def run_merge(keys, q_req, corpus, k, scale=None, n_unique_mode="device", max_unique=0,
+              tiled=False):
     """Run the whole path on the GPU; returns the MergedRetrieval object
-    (outputs still on the device) after a synchronisation."""
+    (outputs still on the device) after a synchronisation.  tiled: score the
+    tiled copy of the corpus (made on the device from the row-major one)."""
     import paper_2607_22578_amd as hs
     dev = device()
     R, d = q_req.shape
     N = corpus.shape[0]
     m = hs.MergedRetrieval(R, d, N, k, enc_code(q_req), enc_code(corpus), device=dev,
-                           max_unique=max_unique)
+                           max_unique=max_unique, tiled_corpus=tiled)
     kd, qd, cd = to_dev(keys), to_dev(q_req), to_dev(corpus)
     sd = to_dev(scale) if scale is not None else None
     st = torch.cuda.current_stream(dev)
+    if tiled:
+        cd = m.tile_corpus(cd, st)
     if n_unique_mode == "host":
         nu = m.dedup(kd, st, host_count=True)
         m.gather_queries(qd, st)

@@ -56,6 +56,22 @@ static hs_plan *plan_of(int64_t R, int64_t d, int64_t N, int k, int qd, int cd, 
     return hs_merge_plan(&desc, &p, ws) == HS_OK ? p : NULL;
 }
 
+static hs_plan *plan_flags(int64_t R, int64_t d, int64_t N, int k, int qd, int cd, int32_t flags,
+                           size_t *ws) {
+    hs_merge_desc desc;
+    memset(&desc, 0, sizeof(desc));
+    desc.n_requests = R;
+    desc.dim = d;
+    desc.n_corpus = N;
+    desc.k = k;
+    desc.query_dtype = qd;
+    desc.corpus_dtype = cd;
+    desc.flags = flags;
+    desc.n_workflows = 1;
+    hs_plan *p = NULL;
+    return hs_merge_plan(&desc, &p, ws) == HS_OK ? p : NULL;
+}
+
 int main(void) {
     size_t ws = 0;
     CHECK(hs_abi_version() == HS_ABI_VERSION);
@@ -110,6 +126,22 @@ int main(void) {
     ACCEPT(hs_score_topk(w, P(F), 10, NULL, P(F), NULL, P(F), P(F), P(F), ws, NULL), 2);
     ACCEPT(hs_score_partial(w, P(F), -1, P(F), P(F), NULL, P(F), ws, NULL), 1);
     ACCEPT(hs_topk_merge(w, -1, P(F), P(F), P(F), P(F), ws, NULL), 1);
+    /* tiled corpus layout */
+    size_t tb = 0;
+    CHECK(hs_corpus_tiled_bytes(w, &tb) == HS_OK && tb == (size_t)2605 * 384 * 768 * 2);
+    REJECT(hs_corpus_tiled_bytes(w, NULL), HS_ERR_INVALID_ARG);
+    REJECT(hs_tile_corpus(w, NULL, P(F + (1ull << 33)), tb, NULL), HS_ERR_INVALID_ARG);
+    REJECT(hs_tile_corpus(w, P(F), P(F + (1ull << 33)), tb - 16, NULL), HS_ERR_INVALID_ARG);
+    REJECT(hs_tile_corpus(w, P(F), P(F + 4096), tb, NULL), HS_ERR_INVALID_ARG);  /* overlap */
+    REJECT(hs_tile_corpus(w, P(F + 8), P(F + (1ull << 33)), tb, NULL), HS_ERR_ALIGNMENT);
+    ACCEPT(hs_tile_corpus(w, P(F), P(F + (1ull << 33)), tb, NULL), 1);
+    hs_plan *wt = plan_flags(2048, 768, 1000000, 10, HS_BF16, HS_BF16, HS_FLAG_TILED_CORPUS, &ws);
+    CHECK(wt != NULL);
+    if (wt) {
+      ACCEPT(hs_score_topk(wt, P(F), 10, NULL, P(F), NULL, P(F), P(F), P(F), ws, NULL), 2);
+      hs_plan_destroy(wt);
+    }
+    CHECK(plan_flags(64, 768, 1000, 10, HS_F32, HS_F32, HS_FLAG_TILED_CORPUS, &ws) == NULL);
     /* the allocation-free variant validates, then finds no GPU here */
     REJECT(hs_score_topk_noalloc(w, P(F), 4096, NULL, P(F), NULL, P(F), P(F), NULL),
            HS_ERR_INVALID_ARG);

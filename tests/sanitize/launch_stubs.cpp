@@ -20,6 +20,9 @@ size_t score_workspace_bytes(int64_t cap, int64_t N, int k, int) {
   return ((size_t)cap * (size_t)k * 64 + 255) & ~(size_t)255;
 }
 size_t priority_workspace_bytes(int64_t cap) { return (size_t)cap * 16; }
+size_t mfma_tiled_bytes(int64_t N, int64_t d, bool fp8) {
+  return (size_t)((N + 383) / 384 * 384) * (size_t)((d + 63) / 64 * 64) * (fp8 ? 1u : 2u);
+}
 size_t cache_layout(int64_t C, int k, void *, CacheView *) {
   return ((size_t)C * (16 + 8 * (size_t)k) + 1023) & ~(size_t)255;
 }
@@ -40,7 +43,8 @@ HS_STUB(launch_gather, const void *, int64_t, int64_t, const void *, int, int64_
 HS_STUB(launch_deliver, const float *, const int32_t *, int64_t, const int32_t *, int64_t, int,
         float *, int32_t *, hipStream_t)
 HS_STUB(launch_score_partial, const void *, const void *, const float *, int64_t, int64_t, int,
-        int64_t, const int64_t *, int64_t, int, void *, hipStream_t)
+        int64_t, const int64_t *, int64_t, int, bool, void *, hipStream_t)
+HS_STUB(launch_tile_corpus, const void *, int64_t, int64_t, bool, void *, hipStream_t)
 HS_STUB(launch_topk_merge, const void *, int64_t, const int64_t *, int64_t, int64_t, int, int,
         float *, int32_t *, hipStream_t)
 HS_STUB(launch_cache_reset, void *, int64_t, int, hipStream_t)

@@ -26,7 +26,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert hs.hs_abi_version() == hs.ABI_VERSION == 2
+    assert hs.hs_abi_version() == hs.ABI_VERSION == 3
     assert hs.hs_status_string(hs.HS_OK) == "HS_OK"
     assert hs.hs_status_string(hs.HS_ERR_WORKSPACE) == "HS_ERR_WORKSPACE"
     assert hs.hs_status_string(99) == "HS_ERR_UNKNOWN"
@@ -61,7 +61,10 @@ def test_plan_ok_and_workspace():
     (dict(query_dtype=hs.HS_F32), hs.HS_ERR_UNSUPPORTED),         # f32 queries + bf16 corpus
     (dict(corpus_dtype=hs.HS_F32), hs.HS_ERR_UNSUPPORTED),        # bf16 queries + f32 corpus
     (dict(max_unique=5000), hs.HS_ERR_INVALID_ARG),
-    (dict(flags=1), hs.HS_ERR_INVALID_ARG),
+    (dict(flags=2), hs.HS_ERR_INVALID_ARG),                       # unknown flag bit
+    (dict(flags=-1), hs.HS_ERR_INVALID_ARG),
+    (dict(flags=hs.HS_FLAG_TILED_CORPUS, query_dtype=hs.HS_F32, corpus_dtype=hs.HS_F32),
+     hs.HS_ERR_UNSUPPORTED),                                      # tiled: BF16/FP8 only
 ])
 def test_plan_rejects(bad, code):
     with pytest.raises(hs.HsError) as e:
@@ -106,6 +109,49 @@ def test_workflow_offsets_rejected(W, off):
 
 
 FAKE = 0x10000000   # never dereferenced: validation fails first
+
+
+def _tiled_size(N, d, esz):
+    # 384-row x 64-column blocks, rows and columns padded with zeros
+    return -(-N // 384) * 384 * (-(-d // 64) * 64) * esz
+
+
+@pytest.mark.parametrize("N,d,cdt,esz", [
+    (1_000_000, 768, hs.HS_BF16, 2), (384, 64, hs.HS_BF16, 2), (385, 72, hs.HS_BF16, 2),
+    (1000, 208, hs.HS_FP8_E4M3, 1), (20_000_000, 512, hs.HS_FP8_E4M3, 1), (0, 128, hs.HS_BF16, 2),
+])
+def test_corpus_tiled_bytes(N, d, cdt, esz):
+    for flags in (0, hs.HS_FLAG_TILED_CORPUS):
+        p = hs.hs_merge_plan(**dict(GOOD, n_corpus=N, dim=d, corpus_dtype=cdt, flags=flags))
+        assert hs.hs_corpus_tiled_bytes(p) == _tiled_size(N, d, esz)
+
+
+def test_tile_corpus_validation():
+    f32 = hs.hs_merge_plan(**dict(GOOD, query_dtype=hs.HS_F32, corpus_dtype=hs.HS_F32))
+    for call in (lambda: hs.hs_corpus_tiled_bytes(f32),
+                 lambda: hs.hs_tile_corpus(f32, FAKE, FAKE, 1 << 40)):
+        with pytest.raises(hs.HsError) as e:
+            call()
+        assert e.value.status == hs.HS_ERR_UNSUPPORTED
+    p = hs.hs_merge_plan(**GOOD)
+    need = hs.hs_corpus_tiled_bytes(p)
+    cases = [
+        ((None, FAKE, need), hs.HS_ERR_INVALID_ARG),            # null corpus
+        ((FAKE, None, need), hs.HS_ERR_INVALID_ARG),            # null tiled buffer
+        ((FAKE, FAKE + (1 << 33), need - 16), hs.HS_ERR_INVALID_ARG),   # buffer too small
+        ((FAKE + 8, FAKE + (1 << 33), need), hs.HS_ERR_ALIGNMENT),
+        ((FAKE, FAKE + (1 << 33) + 4, need), hs.HS_ERR_ALIGNMENT),
+        ((FAKE, FAKE + 4096, need), hs.HS_ERR_INVALID_ARG),     # overlaps the corpus
+        ((FAKE + 4096, FAKE, need), hs.HS_ERR_INVALID_ARG),
+    ]
+    for (c, t, nb), code in cases:
+        with pytest.raises(hs.HsError) as e:
+            hs.hs_tile_corpus(p, c, t, nb)
+        assert e.value.status == code, (c, t, nb)
+    # an empty corpus: nothing to write, nothing enqueued
+    p0 = hs.hs_merge_plan(**dict(GOOD, n_corpus=0))
+    assert hs.hs_corpus_tiled_bytes(p0) == 0
+    hs.hs_tile_corpus(p0, None, None, 0)
 
 
 def test_deliver_validation():

@@ -21,7 +21,7 @@ def test_help_lists_the_modes():
     for flag in ("--steps", "--warmup", "--workload", "--no-merge", "--reuse-store",
                  "--signatures", "--sig-nodes", "--priorities", "--prio-only", "--batch-curve",
                  "--seed", "--oracle-threads", "--raw-ids", "--cpu-sample", "--corpus-rows",
-                 "--batch-sizes", "--graph"):
+                 "--batch-sizes", "--graph", "--corpus-layout"):
         assert flag in r.stdout, flag
     # the no-flag run is the largest single-GPU workload
     assert "mfma4m (default)" in r.stdout
