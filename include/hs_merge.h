@@ -183,7 +183,7 @@ hs_status hs_score_topk(const hs_plan *plan, const void *q_unique, int64_t n_uni
  * the call.  A plan whose score workspace (what hs_merge_plan reports for the
  * score step) exceeds 64 MiB is rejected with HS_ERR_WORKSPACE before
  * anything is enqueued; the 1M-row window (2,048 requests, d = 768, k = 10)
- * needs about 50 MiB.  Every call on one GPU uses that GPU's one array, which
+ * needs about 62 MiB.  Every call on one GPU uses that GPU's one array, which
  * keeps the previous call's contents (each call writes everything it reads
  * before reading it): calls that overlap in time on one GPU -- on different
  * streams, or from host threads without ordering -- race and give wrong

@@ -26,7 +26,7 @@ hipError_t launch_deliver(const float *ts, const int32_t *ti, int64_t rows, cons
                           int64_t R, int k, float *os, int32_t *oi, hipStream_t st);
 size_t noalloc_scratch_bytes();
 hipError_t noalloc_scratch(void **ptr);
-size_t score_workspace_bytes(int64_t cap, int64_t N, int k, int corpus_dtype);
+size_t score_workspace_bytes(int64_t cap, int64_t N, int64_t d, int k, int corpus_dtype);
 hipError_t launch_score_partial(const void *q, const void *corpus, const float *scale, int64_t N,
                                 int64_t d, int k, int64_t n_unique, const int64_t *nu_dev,
                                 int64_t cap, int corpus_dtype, bool tiled, void *part,
@@ -181,7 +181,7 @@ hs_status hs_merge_plan(const hs_merge_desc *desc, hs_plan **plan, size_t *works
   p->d.workflow_offsets = nullptr;
   p->cap = d.max_unique > 0 ? d.max_unique : d.n_requests;
   p->ws_dedup = hs::dedup_workspace_bytes(d.n_requests);
-  p->ws_score = hs::score_workspace_bytes(p->cap, d.n_corpus, d.k, d.corpus_dtype);
+  p->ws_score = hs::score_workspace_bytes(p->cap, d.n_corpus, d.dim, d.k, d.corpus_dtype);
   p->ws_prio = hs::priority_workspace_bytes(p->cap);
   p->ws_total = p->ws_dedup > p->ws_score ? p->ws_dedup : p->ws_score;
   if (p->ws_prio > p->ws_total) p->ws_total = p->ws_prio;

@@ -496,6 +496,8 @@ int persistent_grid(bool mfma) {
 }
 
 size_t mfma_partial_bytes(int64_t cap, int64_t N, int k, int grid_max);
+size_t mfma_qtile_offset(int64_t cap, int64_t N, int k, int grid_max);
+size_t mfma_qtile_bytes(int64_t cap, int64_t d);
 size_t mfma_part_offset(int64_t cap, int64_t N, int k, int grid_max);
 void mfma_split_params(int *mq, int *nc, int64_t *smax, int k);
 hipError_t launch_score_mfma(const void *q, const void *corpus, const float *scale, int64_t N,
@@ -518,9 +520,9 @@ static size_t partial_bytes(int64_t cap, int64_t N, int mq, int nc, int k) {
   return (best + 255) & ~(size_t)255;
 }
 
-size_t score_workspace_bytes(int64_t cap, int64_t N, int k, int corpus_dtype) {
+size_t score_workspace_bytes(int64_t cap, int64_t N, int64_t d, int k, int corpus_dtype) {
   if (corpus_dtype == HS_F32) return partial_bytes(cap, N, kVMQ, kVNC, k);
-  return mfma_partial_bytes(cap, N, k, kGridMax);
+  return mfma_qtile_offset(cap, N, k, kGridMax) + mfma_qtile_bytes(cap, d);
 }
 
 template <typename K>

@@ -934,9 +934,11 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
     }
     float thr_r[kMQB];   // (read from L.thr after the prologue barrier)
 
+    // the query tile's rows in the tiled order of tile_queries_kernel: stage
+    // s of the tile is the 16 KiB block s, already in LDS order
     const i32x4m qrs =
-        make_rsrc((const unsigned char *)a.q + (int64_t)it.qbase * d * 2,
-                  (uint32_t)(it.qvalid * d * 2));
+        make_rsrc((const unsigned char *)a.q + (int64_t)(it.qbase / kMMQ) * nch * G::bbytes,
+                  (uint32_t)(nch * G::bbytes));
 
     // copy stream: next chunk to issue.  A chunk is copied in two parts:
     // issue_a copies the corpus rows of this wave (the only wave that reads
@@ -988,30 +990,23 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
       for (int j = 0; j < G::adma; ++j) issue_a_j(ca, j);
     };
     struct CopyB {
-      uint32_t lds, voff, voff1;
+      uint32_t lds, voff;
     };
-    // query part of the next chunk: pieces past d (a partial last stage),
-    // and every piece once the stream has ended, read as zeros through an
-    // offset past the range
+    // query part of the next chunk: this wave's bdma consecutive KiB of the
+    // stage's block (queries past n_u and columns past d are zeros there);
+    // once the stream has ended, zeros through an offset past the range
     auto prep_b = [&]() __attribute__((always_inline)) {
       CopyB cb;
-      constexpr int PB = G::bpieces;
       const int ln = opaque(lane);
-      const int bpiece = swz_slot<PB>(ln % PB, ln / PB);
-      const int bpiece1 = swz_slot<PB>(ln % PB, 8 + ln / PB);
       const int wvs = __builtin_amdgcn_readfirstlane(wv);
-      cb.voff = i_left > 0 && i_kc + bpiece * 8 < d
-                    ? (uint32_t)(((wvs * G::bdma * (64 / PB) + ln / PB) * d + bpiece * 8 + i_kc) * 2)
-                    : 0x80000000u;
-      cb.voff1 = i_left > 0 && i_kc + bpiece1 * 8 < d
-                    ? (uint32_t)(((wvs * G::bdma * (64 / PB) + ln / PB) * d + bpiece1 * 8 + i_kc) * 2)
+      cb.voff = i_left > 0
+                    ? (uint32_t)((i_kc / kMKC) * G::bbytes + wvs * G::bdma * 1024 + ln * 16)
                     : 0x80000000u;
       cb.lds = (uint32_t)(uintptr_t)(L.ring + i_slot * G::stage + G::abytes) + wvs * G::bdma * 1024;
       return cb;
     };
     auto issue_b_j = [&](const CopyB &cb, int j) __attribute__((always_inline)) {
-      constexpr int PB = G::bpieces;
-      dma16s(qrs, cb.lds + j * 1024, ((j & 1) ? cb.voff1 : cb.voff) + (uint32_t)(j * (64 / PB) * d * 2));
+      dma16s(qrs, cb.lds + j * 1024, cb.voff + (uint32_t)(j * 1024));
     };
     auto extras_advance = [&]() __attribute__((always_inline)) {
       if (i_left <= 0) return;
@@ -1437,6 +1432,45 @@ __global__ __launch_bounds__(256) void tile_corpus_kernel(const unsigned char *_
   }
 }
 
+// The distinct queries in the same order, per query tile: tile u (queries
+// [128 u, 128 u + 128)) and stage s form the 16 KiB block u * nch + s, row r
+// of the tile at r * 128 bytes with its pieces in the swizzled slots; queries
+// past n_u and columns past d are zeros.  Written into the score workspace at
+// the start of every score call (n_u * d * 2 bytes read, the tiles' bytes
+// written), so that the score kernel's query copies read consecutive KiB too.
+__global__ __launch_bounds__(256) void tile_queries_kernel(
+    const unsigned char *__restrict__ q, int64_t n_unique, const int64_t *__restrict__ nu_dev,
+    int64_t cap, int64_t d, int nch, uint4 *__restrict__ dst) {
+  constexpr int PB = Geo<false>::bpieces;
+  constexpr int per_stage = Geo<false>::bbytes / 16;
+  const int64_t nu = read_nu(n_unique, nu_dev, cap);
+  const int64_t npieces = (nu + kMMQ - 1) / kMMQ * nch * per_stage;
+  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < npieces;
+       p += (int64_t)gridDim.x * 256) {
+    const int64_t blk = p / per_stage;
+    const int in = (int)(p - blk * per_stage);
+    const int64_t u = blk / nch;
+    const int s = (int)(blk - u * nch);
+    const int r = in / PB;
+    const int piece = swz_slot<PB>(in % PB, r);
+    const int64_t row = u * kMMQ + r;
+    const int64_t col = (int64_t)s * kMKC + piece * 8;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (row < nu && col < d) v = *reinterpret_cast<const uint4 *>(q + (row * d + col) * 2);
+    dst[p] = v;
+  }
+}
+
+// Bytes of the tiled queries for up to cap distinct queries.
+size_t mfma_qtile_bytes(int64_t cap, int64_t d) {
+  return (size_t)((cap + kMMQ - 1) / kMMQ) * (size_t)((d + kMKC - 1) / kMKC) * Geo<false>::bbytes;
+}
+
+// Offset of the tiled queries in the score workspace (after the partial lists).
+size_t mfma_qtile_offset(int64_t cap, int64_t N, int k, int grid_max) {
+  return (mfma_partial_bytes(cap, N, k, grid_max) + 255) & ~(size_t)255;
+}
+
 size_t mfma_tiled_bytes(int64_t N, int64_t d, bool fp8) {
   const int64_t tiles = (N + kMNC - 1) / kMNC, nch = (d + kMKC - 1) / kMKC;
   return (size_t)(tiles * nch) * (size_t)(fp8 ? Geo<true>::abytes : Geo<false>::abytes);
@@ -1467,8 +1501,18 @@ hipError_t launch_score_mfma(const void *q, const void *corpus, const float *sca
   uint32_t *lvl = (uint32_t *)((unsigned char *)ws + mfma_thr_bytes(cap) +
                                mfma_lmax_bytes(cap, N, k, kMGridMax));
   void *part = (unsigned char *)ws + mfma_part_offset(cap, N, k, kMGridMax);
+  void *qt = (unsigned char *)ws + mfma_qtile_offset(cap, N, k, kMGridMax);
+  if (cap > 0) {
+    const int nch = (int)((d + kMKC - 1) / kMKC);
+    const int64_t want = (int64_t)(mfma_qtile_bytes(cap, d) / 16 + 255) / 256;
+    const unsigned blocks = (unsigned)(want < 2048 ? want : 2048);
+    hipLaunchKernelGGL(tile_queries_kernel, dim3(blocks), dim3(256), 0, st,
+                       (const unsigned char *)q, n_unique, nu_dev, cap, d, nch, (uint4 *)qt);
+    hipError_t e0 = hipGetLastError();
+    if (e0 != hipSuccess) return e0;
+  }
   MfmaArgs a;
-  a.q = q;
+  a.q = qt;
   a.corpus = corpus;
   a.scale = scale;
   a.N = N;

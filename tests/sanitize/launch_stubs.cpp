@@ -15,8 +15,9 @@ int hs_stub_launches = 0;
 namespace hs {
 struct CacheView;
 size_t dedup_workspace_bytes(int64_t R) { return R <= 4096 ? 0 : (size_t)R * 32; }
-size_t score_workspace_bytes(int64_t cap, int64_t N, int k, int) {
+size_t score_workspace_bytes(int64_t cap, int64_t N, int64_t d, int k, int) {
   (void)N;
+  (void)d;
   return ((size_t)cap * (size_t)k * 64 + 255) & ~(size_t)255;
 }
 size_t priority_workspace_bytes(int64_t cap) { return (size_t)cap * 16; }
