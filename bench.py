@@ -44,12 +44,13 @@ def traffic_file(workload: str) -> str:
 
 KERNEL_SOURCES = ["paper_2607_22578_amd/csrc/score_mfma.hip", "paper_2607_22578_amd/csrc/score.hip",
                   "paper_2607_22578_amd/csrc/common.h"]
-# The score step (hs_score_partial) is three launches on one stream: the seed
-# pass, the seed selection (which also restarts the shared thresholds) and the
-# main pass.  Its HIP-event duration is the sum of those kernels' durations.
+# The score step (hs_score_partial) is four launches on one stream: the query
+# tiling, the seed pass, the seed selection (which also restarts the shared
+# thresholds) and the main pass.  Its HIP-event duration is the sum of those
+# kernels' durations.
 EV_EVERY = 4
-SCORE_STEP = ("score step = score_mfma_dma (seed pass) + mfma_seed_kernel + "
-              "score_mfma_dma (main pass)")
+SCORE_STEP = ("score step = tile_queries_kernel + score_mfma_dma (seed pass) + mfma_seed_kernel "
+              "+ score_mfma_dma (main pass)")
 SCORE_STEP_VALU = "score step = score_partial_valu (fp32, vector units)"
 
 

@@ -1,6 +1,6 @@
 """Parity at the full workload sizes, in the launch configuration the
 benchmark times (whole path on one stream, distinct count kept on the
-device).  Dedup, gathers and delivery are checked bit-exactly in full; the
+device, corpus in the tiled layout).  Dedup, gathers and delivery are checked bit-exactly in full; the
 exact top-k is checked for distinct queries spread over every block of 128
 consecutive distinct queries (all of them on the 1M-row workload), and for a
 seeded sample of requests against an independent, unmerged retrieval of each
@@ -26,7 +26,7 @@ def _run(name):
         note(f"{name}: generating")
         w = synth.make(name)
         note(f"{name}: R={w.R} N={w.n_corpus} d={w.dim} k={w.k} corpus={w.corpus.dtype}")
-        m = run_merge(w.keys, w.q_req, w.corpus, w.k, scale=w.scale)
+        m = run_merge(w.keys, w.q_req, w.corpus, w.k, scale=w.scale, tiled=True)
         ref = check_dedup(m, w.keys)
         note(f"{name}: dedup exact, n_u={ref['n_unique']}")
         check_delivery(m, w.R)
