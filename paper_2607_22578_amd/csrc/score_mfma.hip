@@ -95,6 +95,14 @@ __host__ __device__ __forceinline__ int seed_tiles(int k, int64_t ntiles, int64_
   if (t > kSeedTilesMax) t = kSeedTilesMax;
   return t < 1 ? 1 : (int)t;
 }
+// Slices that take part in the seed sample: one in every seed_stride(S), at
+// most kSeedSlices of them.  A single query tile runs as up to 256 slices, and
+// the seed pass (one tile per workgroup, all at once) then reads that many
+// tiles of the corpus; half of them are as good a sample for the seed.
+constexpr int kSeedSlices = 128;
+__host__ __device__ __forceinline__ int64_t seed_stride(int64_t S) {
+  return S > kSeedSlices ? (S + kSeedSlices - 1) / kSeedSlices : 1;
+}
 constexpr int kMSplitMaxSK = 8192;       // bound on S*k (merge list length)
 constexpr int kMRowsW = 32 * kMRB;       // rows per wave in a tile
 constexpr int kMSS = kMNC + 128 - kMRowsW;  // row-scale slot stride (floats): the
@@ -905,6 +913,16 @@ __device__ __forceinline__ void run_item(const MfmaArgs &a, const MLds &L, const
     it.qvalid = (int)(nu - it.qbase < kMMQ ? nu - it.qbase : kMMQ);
     const int ntl = t1 - t0;
     const int T = ntl * nch;
+    if constexpr (SEED) {
+      if (it.s % seed_stride(it.S) != 0) {   // not sampled: no lane maxima
+        const int per = it.T * kMLanesQ;
+        for (int e = tid; e < it.qvalid * per; e += kMT) {
+          const int qq = e / per, r = e - qq * per;
+          a.lmax[((int64_t)(it.qbase + qq) * it.S + it.s) * per + r] = 0u;
+        }
+        return;
+      }
+    }
 
     // per-item state
     if (tid < kMMQ) {
@@ -1539,9 +1557,10 @@ hipError_t launch_score_mfma(const void *q, const void *corpus, const float *sca
     return ll ? launch_mfma(score_mfma_dma<false, true, false>, a.grid, lds, a, st)
               : launch_mfma(score_mfma_dma<false, false, false>, a.grid, lds, a, st);
   };
-  // Seed pass: score the first T tiles of every slice and keep only lane
-  // maxima; their k-th largest per query (a lower bound of the query's k-th
-  // best over the corpus, taken over a sample of S T tiles spread over it)
+  // Seed pass: score the first T tiles of every sampled slice (all slices, or
+  // one in seed_stride(S)) and keep only lane maxima; their k-th largest per
+  // query (a lower bound of the query's k-th best over the corpus, taken over
+  // a sample of tiles spread over it)
   // seeds the shared thresholds.  The main pass then scores every tile with
   // lists that stay nearly untouched from the first tile on.
   hipError_t e = run(true);

@@ -3,7 +3,8 @@ the oracle (acceptance rule of oracle/accept.py): dimensions that leave a
 partial last K stage (the copies read zeros past d), corpora smaller than
 one 384-row tile or with a ragged last tile, k-lists held in global memory
 instead of LDS, k too large for the first-pass threshold seed, a seed that
-samples several tiles per slice (k > 48), items of later rounds that start
+samples several tiles per slice (k > 48) or one slice in two (a single
+query tile over 256 slices), items of later rounds that start
 from the order statistics of finished slices, and a merge with more
 survivors than it ranks by counting (it sorts them)."""
 import numpy as np
@@ -100,6 +101,26 @@ def test_large_k_seed_samples_several_tiles(enc):
     sel = np.random.default_rng(11).choice(ref["n_unique"], size=40, replace=False)
     check_unique_topk(m, ref, q, c, k, scale=sc if enc == "fp8" else None, sel=np.sort(sel))
     check_delivery(m, w.R)
+
+
+@pytest.mark.parametrize("enc,k", [("bf16", 10), ("fp8", 10), ("bf16", 64)])
+def test_seed_sample_every_second_slice(enc, k):
+    # one query tile (the first 300 requests of the 1M-row stream, fewer than
+    # 128 distinct) over 150,000 rows: 256 slices of one or two tiles, of
+    # which the seed pass samples every second one (the others contribute
+    # no lane maxima); bf16 with k = 64 keeps its lists in global memory
+    w = synth.make("ridge1m", n_corpus=1, with_corpus=False)
+    d, n_corpus = 64, 150_000
+    keys = w.keys[:300]
+    q, _ = synth.gaussian_rows(w.seed, synth.S_QUERY, 0, d, "bf16", row_ids=w.template_ids[:300])
+    c, sc = synth.gaussian_rows(w.seed, synth.S_CORPUS, n_corpus, d, enc)
+    scale = sc if enc == "fp8" else None
+    note(f"{enc} k={k} N={n_corpus} d={d}: seed sample of 128 of 256 slices")
+    m = run_merge(keys, q, c, k, scale=scale)
+    ref = check_dedup(m, keys)
+    assert ref["n_unique"] <= 128
+    check_unique_topk(m, ref, q, c, k, scale=scale)
+    check_delivery(m, 300)
 
 
 @pytest.mark.parametrize("enc", ["bf16", "fp8"])
