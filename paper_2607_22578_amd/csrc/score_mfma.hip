@@ -22,12 +22,15 @@
 // for bf16, three for fp8), one K range of 64 per stage, written by
 // buffer_load ... lds (asynchronous copies from global memory straight into
 // LDS, no registers).  A bf16 corpus row contributes one 128-byte line per
-// stage (fp8: 64 bytes).  Every copy goes through a buffer descriptor whose
-// range covers exactly the valid rows of the tile (or query tile): rows past
-// N or past n_u, and the part of a last stage past d, read as zeros, so there
-// are no bounds branches and no access outside the operands.  Rows are stored
-// as 16-byte pieces with an XOR swizzle so that fragment reads (ds_read_b128)
-// are bank-conflict free.  Inside one MFMA the K order is free as long as
+// stage (fp8: 64 bytes).  Rows are stored in LDS as 16-byte pieces with an
+// XOR swizzle so that fragment reads (ds_read_b128) are bank-conflict free.
+// The query rows, and the corpus when it is given in the tiled layout, are
+// kept in global memory in exactly that LDS order (tile_queries_kernel,
+// tile_corpus_kernel), zero-padded past n_u, N and d, so every copy reads
+// 1 KiB of consecutive bytes; a row-major corpus is copied as row pieces
+// through a descriptor whose range covers the tile's valid rows (rows past N
+// read as zeros).  Either way there are no bounds branches and no access
+// outside the operands.  Inside one MFMA the K order is free as long as
 // both operands agree; each lane takes the K slice that makes its fp8 corpus
 // piece one 16-byte read.
 //
@@ -49,8 +52,9 @@
 // reserves the slots), merged into the query's sorted k-list when a queue
 // is due.  Thresholds come from lower bounds of the query's final k-th best
 // score: the slice's own k-list; a seed, the k-th largest of the lane maxima
-// of a first pass over the first tiles of every slice (a sample spread over
-// the corpus); the order statistics of the slices finished so far; and the
+// of a first pass over the first tiles of the slices (at most 128 of them:
+// a sample spread over the corpus); the order statistics of the slices
+// finished so far; and the
 // largest bound any slice of the query has published so far (a per-query
 // array in the workspace, read asynchronously with each tile's copies).
 // Keys order by (score desc, row asc): ties go to the lower
