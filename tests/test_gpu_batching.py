@@ -15,18 +15,21 @@ from gpu_harness import check_dedup, check_unique_topk, device, note, to_dev
 pytestmark = pytest.mark.gpu
 
 
-def _setup(n_corpus=20_000, enc="bf16"):
+def _setup(n_corpus=20_000, enc="bf16", tiled=False):
     import paper_2607_22578_amd as hs
     dev = device()
     w = synth.make("ridge1m", n_corpus=1, with_corpus=False)
     c, sc = synth.gaussian_rows(w.seed, synth.S_CORPUS, n_corpus, w.dim, enc)
     m = hs.MergedRetrieval(w.R, w.dim, n_corpus, w.k, hs.HS_BF16,
-                           hs.HS_BF16 if enc == "bf16" else hs.HS_FP8_E4M3, device=dev)
+                           hs.HS_BF16 if enc == "bf16" else hs.HS_FP8_E4M3, device=dev,
+                           tiled_corpus=tiled)
     st = torch.cuda.current_stream(dev)
     kd, qd = to_dev(w.keys), to_dev(w.q_req)
     nu = m.dedup(kd, st, host_count=True)
     m.gather_queries(qd, st)
     cd = to_dev(c)
+    if tiled:
+        cd = m.tile_corpus(cd, st)
     sd = to_dev(sc) if sc is not None else None
     return w, m, c, sc, cd, sd, nu, st
 
@@ -37,9 +40,12 @@ def _snapshot(m, nu):
             m.topk_index[:nu].cpu().numpy().copy())
 
 
-@pytest.mark.parametrize("enc", ["bf16", "fp8"])
-def test_sequential_chunks_equal_one_batch(enc):
-    w, m, c, sc, cd, sd, nu, st = _setup(enc=enc)
+@pytest.mark.parametrize("enc,tiled", [("bf16", False), ("fp8", False), ("bf16", True),
+                                       ("fp8", True)])
+def test_sequential_chunks_equal_one_batch(enc, tiled):
+    # (sub-batches start at any query row, so the query tiling of each call
+    # starts there too; tiled: the corpus in the tiled layout)
+    w, m, c, sc, cd, sd, nu, st = _setup(enc=enc, tiled=tiled)
     m.score_chunked(cd, nu, nu, sd, st)
     s1, i1 = _snapshot(m, nu)
     ref = check_dedup(m, w.keys)
