@@ -218,7 +218,9 @@ hs_status hs_tile_corpus(const hs_plan *plan, const void *corpus, void *tiled,
  * one persistent kernel, each workgroup keeping the k best (score, row) pairs
  * of its corpus slice per query; the per-slice lists go to the workspace
  * (for BF16/FP8 corpora, together with a per-query lower bound of the k-th
- * best score, which phase 2 uses to drop list entries early).
+ * best score, which phase 2 uses to drop list entries early; the workspace
+ * also holds a copy of the distinct queries in the kernel's tiled order,
+ * written by the call itself, so q_unique is only read).
  * Arguments as for hs_score_topk. */
 hs_status hs_score_partial(const hs_plan *plan, const void *q_unique, int64_t n_unique,
                            const int64_t *n_unique_dev, const void *corpus,
