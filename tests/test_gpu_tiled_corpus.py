@@ -2,7 +2,8 @@
 copy byte for byte against a numpy re-layout written here from the layout's
 definition in hs_merge.h, and the score step on it against the row-major
 corpus (bit-identical outputs: the kernel's LDS contents are the same) and
-against the oracle, on ragged corpora, partial last K stages, k-lists in LDS
+against the oracle, on ragged corpora, partial last K stages, the largest
+dimension (d = 16,384), k-lists in LDS
 and in global memory, several query tiles and the no-allocation entry point."""
 import numpy as np
 import pytest
@@ -116,3 +117,17 @@ def test_tiled_noalloc_and_host_count():
     np.testing.assert_array_equal(ts.cpu().numpy().view(np.uint32),
                                   a.topk_score[:nu].cpu().numpy().view(np.uint32))
     np.testing.assert_array_equal(ti.cpu().numpy(), a.topk_index[:nu].cpu().numpy())
+
+
+@pytest.mark.parametrize("enc", ["bf16", "fp8"])
+def test_max_dimension_both_layouts(enc):
+    # d = 16,384 (the largest the plan accepts): 256 stages per tile, 12 MiB
+    # bf16 tiles, over a ragged corpus of four tiles
+    w, q, c, sc = _stream(1500, 16384, enc, workload="tiny")
+    note(f"max dimension {enc}")
+    rows = run_merge(w.keys, q, c, w.k, scale=sc)
+    tiled = run_merge(w.keys, q, c, w.k, scale=sc, tiled=True)
+    _same_outputs(rows, tiled, w.R)
+    ref = check_dedup(tiled, w.keys)
+    check_unique_topk(tiled, ref, q, c, w.k, scale=sc)
+    check_delivery(tiled, w.R)
