@@ -94,12 +94,13 @@ def test_k_values(k):
     check_delivery(m, w.R)
 
 
+@pytest.mark.parametrize("tiled", [False, True])
 @pytest.mark.parametrize("N", [0, 1, 7, 129])
-def test_k_exceeds_corpus_pads(N):
+def test_k_exceeds_corpus_pads(N, tiled):
     w = synth.make("ridge1m", n_corpus=max(N, 1))
     corpus = w.corpus[:N]
     k = 10
-    m = run_merge(w.keys, w.q_req, corpus, k)
+    m = run_merge(w.keys, w.q_req, corpus, k, tiled=tiled)
     ref = check_dedup(m, w.keys)
     if N > 0:
         check_unique_topk(m, ref, w.q_req, corpus, k)
