@@ -87,10 +87,10 @@ constexpr int kMLanesQ = kMW * 2;        // lanes holding one query in a tile
 // sizeable fraction of the sample): a sample of M rows lets about N k / M rows
 // of the corpus pass it, each a list insertion, and with many slices the
 // lists do not fill before their slice ends, so their own minima never take
-// over.  T therefore grows to 32 as long as the sample stays within 1/16 of
+// over.  T therefore grows to 20 as long as the sample stays within 1/16 of
 // the slice's tiles and within kSeedMax values.
 constexpr int kSeedMax = 16384;
-constexpr int kSeedTilesMax = 32;
+constexpr int kSeedTilesMax = 20;
 __host__ __device__ __forceinline__ int seed_tiles(int k, int64_t ntiles, int64_t S) {
   if (k <= 48 || S < 1) return 1;
   int64_t t = ntiles / (S * 16);
