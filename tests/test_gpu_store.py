@@ -20,18 +20,21 @@ N_CORPUS = 12_000     # 31 full 384-row tiles and a ragged one
 
 
 def _run(capacity, n_windows, k=10, enc="bf16", n_corpus=N_CORPUS, workload="ridge1m",
-         n_check=None):
+         n_check=None, tiled=False):
     import paper_2607_22578_amd as hs
     dev = device()
     wins = synth.window_stream(workload, n_windows)
     d = wins[0].dim
     c, sc = synth.gaussian_rows(wins[0].seed, synth.S_CORPUS, n_corpus, d, enc)
     R = wins[0].R
-    m = hs.MergedRetrieval(R, d, n_corpus, k, enc_code(wins[0].q_req), enc_code(c), device=dev)
+    m = hs.MergedRetrieval(R, d, n_corpus, k, enc_code(wins[0].q_req), enc_code(c), device=dev,
+                           tiled_corpus=tiled)
     m.enable_cache(capacity)
     cd = to_dev(c)
     sd = to_dev(sc) if sc is not None else None
     st = torch.cuda.current_stream(dev)
+    if tiled:
+        cd = m.tile_corpus(cd, st)
     model = store.StoreModel(capacity)
     last = {}          # key -> (scores, indices) the device computed at its last miss
     n_hits = []
@@ -84,6 +87,13 @@ def test_one_entry_store():
 
 def test_fp8_corpus_and_global_lists():
     _run(1024, 2, k=40, enc="fp8")
+
+
+@pytest.mark.parametrize("enc", ["bf16", "fp8"])
+def test_reuse_on_the_tiled_corpus(enc):
+    # the store with the corpus in the tiled layout, as the benchmark runs it
+    hits = _run(4096, 3, enc=enc, tiled=True)
+    assert hits[0] == 0 and hits[1] > 0
 
 
 def test_first_window_equals_uncached_path():
