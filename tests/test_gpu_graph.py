@@ -25,8 +25,8 @@ def _to_dev(a, dev):
     return torch.from_numpy(a).to(dev)
 
 
-@pytest.mark.parametrize("enc", ["bf16", "fp8"])
-def test_window_graph_replays_match_eager(enc):
+@pytest.mark.parametrize("enc,tiled", [("bf16", False), ("fp8", False), ("bf16", True)])
+def test_window_graph_replays_match_eager(enc, tiled):
     dev = device()
     wins = synth.window_stream("ridge1m", 4)
     w0 = wins[0]
@@ -35,7 +35,10 @@ def test_window_graph_replays_match_eager(enc):
     c, sc = synth.gaussian_rows(w0.seed, synth.S_CORPUS, n_corpus, d, enc)
     corpus, scale = _to_dev(c, dev), (_to_dev(sc, dev) if sc is not None else None)
     cdt = hs.HS_FP8_E4M3 if enc == "fp8" else hs.HS_BF16
-    m = hs.MergedRetrieval(w0.R, d, n_corpus, k, hs.HS_BF16, cdt, device=dev)
+    m = hs.MergedRetrieval(w0.R, d, n_corpus, k, hs.HS_BF16, cdt, device=dev, tiled_corpus=tiled)
+    if tiled:   # (made once, outside the captured window)
+        corpus = m.tile_corpus(corpus)
+        torch.cuda.synchronize(dev)
     keys = _to_dev(wins[0].keys, dev).clone()
     q_req = _to_dev(wins[0].q_req, dev).clone()
     s = torch.cuda.Stream(dev)   # default priority
